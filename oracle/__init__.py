@@ -1,0 +1,14 @@
+"""Plain fp64 CPU oracle for block-diffusion masked attention.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package; the product path
+(the HIP library and its Python binding) never calls it.
+"""
+from .bd_attn_oracle import (  # noqa: F401
+    block_index,
+    visibility_mask,
+    allowed_count,
+    forward,
+    backward,
+    probabilities,
+)

@@ -1,0 +1,183 @@
+"""fp64 reference for block-diffusion masked attention over a packed [x_t | x_0] sequence.
+
+TEST INFRASTRUCTURE ONLY: this module is the oracle that the HIP library is
+checked against.  Only tests, the smoke check and the benchmark's CPU-baseline
+leg use it.  It shares no code with the HIP path and imports nothing from it.
+
+What it computes (DiRL, arXiv 2512.22234):
+
+* Section 2.1, Eq. 1: a sequence of L tokens is cut into K blocks of S tokens
+  and modelled autoregressively across blocks, so the clean copy x_0 attends
+  block-causally: clean block k sees clean blocks 0..k.
+* Section 2.1, Eq. 2: the noisy state of block k is denoised in parallel from
+  its own noisy tokens (bidirectionally) and the clean history b^{<k}: a noisy
+  token of block k sees the noisy tokens of block k and the clean tokens of
+  blocks 0..k-1.  A clean token never sees a noisy one.
+* Section 4.1 (and the caption of Fig. 4): DiRL repeats the whole sequence
+  (prompt and output alike) and trains with one regular mask, so attention
+  runs over the 2L tokens [x_t | x_0] (noisy copy first) with the mask above
+  and no prompt/output distinction.
+
+Readings taken where the paper is silent: positions p < L are noisy, block
+index b(p) = (p mod L) div S (a shorter last block when S does not divide L),
+softmax scale defaults to 1/sqrt(D), LSE is the natural-log log-sum-exp of the
+scaled scores over visible keys, query head h uses KV head h div (Hq/Hkv).
+
+Everything is the plain definition written out in float64: the explicit
+2L x 2L mask, dense scores, softmax, and the textbook softmax-attention
+vector-Jacobian product.  Rows are processed in chunks only to bound memory;
+the arithmetic per row is unchanged.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+def block_index(L: int, S: int) -> np.ndarray:
+    """b(p) = (p mod L) div S for every packed position p in [0, 2L) (Section 2.1)."""
+    p = np.arange(2 * L)
+    return (p % L) // S
+
+
+def visibility_mask(L: int, S: int) -> np.ndarray:
+    """Boolean [2L, 2L] mask, M[q, k] true iff query q may attend to key k.
+
+    Noisy query (q < L): noisy key of the same block (Eq. 2, bidirectional
+    within the block) or clean key of an earlier block (Eq. 2's b^{<k}).
+    Clean query: clean key of the same or an earlier block (Eq. 1).
+    Clean query, noisy key: never.
+    """
+    if L < 1 or S < 1:
+        raise ValueError("L and S must be >= 1")
+    p = np.arange(2 * L)
+    noisy = p < L
+    b = (p % L) // S
+    nq, nk = noisy[:, None], noisy[None, :]
+    bq, bk = b[:, None], b[None, :]
+    M = (nq & nk & (bq == bk)) | (nq & ~nk & (bk < bq)) | (~nq & ~nk & (bk <= bq))
+    # every row sees at least its own position
+    assert M.any(axis=1).all()
+    return M
+
+
+def allowed_count(L: int, S: int) -> int:
+    """Number of visible (query, key) pairs for one (batch, head)."""
+    return int(visibility_mask(L, S).sum())
+
+
+def _as64(x) -> np.ndarray:
+    if hasattr(x, "detach"):  # torch tensor
+        x = x.detach().to("cpu").double().numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def _check_shapes(Q, K, V, L):
+    if Q.ndim != 4 or K.ndim != 4 or V.shape != K.shape:
+        raise ValueError("Q [B,Hq,2L,D], K/V [B,Hkv,2L,D] expected")
+    B, Hq, N, D = Q.shape
+    if N != 2 * L or K.shape[0] != B or K.shape[2] != N or K.shape[3] != D:
+        raise ValueError("inconsistent shapes")
+    Hkv = K.shape[1]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    return B, Hq, Hkv, D
+
+
+def _rows(N: int, chunk: int):
+    for r0 in range(0, N, chunk):
+        yield r0, min(N, r0 + chunk)
+
+
+def _softmax_rows(Zc: np.ndarray, Mc: np.ndarray):
+    """Masked row softmax of a chunk of scores: returns P, row max, row sum."""
+    Z = np.where(Mc, Zc, -np.inf)
+    m = Z.max(axis=1, keepdims=True)
+    E = np.exp(Z - m)
+    l = E.sum(axis=1, keepdims=True)
+    return E / l, m, l
+
+
+def forward(Q, K, V, L: int, S: int, scale: float | None = None,
+            heads=None, row_chunk: int = 1024):
+    """O = softmax(scale * Q K^T masked) V and LSE = log sum exp of the masked scores.
+
+    heads: optional iterable of (b, hq) pairs to compute; other heads are NaN.
+    Returns (O [B,Hq,2L,D], LSE [B,Hq,2L]) in float64.
+    """
+    Q, K, V = _as64(Q), _as64(K), _as64(V)
+    B, Hq, Hkv, D = _check_shapes(Q, K, V, L)
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = visibility_mask(L, S)
+    N = 2 * L
+    O = np.full(Q.shape, np.nan)
+    LSE = np.full(Q.shape[:3], np.nan)
+    todo = [(b, h) for b in range(B) for h in range(Hq)] if heads is None else list(heads)
+    for b, h in todo:
+        g = h // G
+        for r0, r1 in _rows(N, row_chunk):
+            Zc = scale * (Q[b, h, r0:r1] @ K[b, g].T)
+            P, m, l = _softmax_rows(Zc, M[r0:r1])
+            O[b, h, r0:r1] = P @ V[b, g]
+            LSE[b, h, r0:r1] = (m + np.log(l))[:, 0]
+    return O, LSE
+
+
+def probabilities(Q, K, L: int, S: int, scale: float | None = None) -> np.ndarray:
+    """Dense attention probabilities P [B,Hq,2L,2L] (small shapes only)."""
+    Q, K = _as64(Q), _as64(K)
+    B, Hq, Hkv, D = _check_shapes(Q, K, K, L)
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = visibility_mask(L, S)
+    P = np.empty((B, Hq, 2 * L, 2 * L))
+    for b in range(B):
+        for h in range(Hq):
+            P[b, h] = _softmax_rows(scale * (Q[b, h] @ K[b, h // G].T), M)[0]
+    return P
+
+
+def backward(dO, Q, K, V, L: int, S: int, scale: float | None = None,
+             groups=None, row_chunk: int = 1024):
+    """Gradients of <dO, O> with respect to Q, K and V.
+
+    The textbook vector-Jacobian product of softmax attention:
+        dV = P^T dO,  dP = dO V^T,  Delta = rowsum(dO * O),
+        dS = P * (dP - Delta),  dQ = scale dS K,  dK = scale dS^T Q,
+    with P the masked softmax of the forward pass, and dK/dV of a KV head
+    summed over the query heads that share it.
+
+    groups: optional iterable of (b, hkv) pairs; only those KV heads and their
+    query heads are computed, everything else is NaN.
+    Returns (dQ, dK, dV) in float64.
+    """
+    dO, Q, K, V = _as64(dO), _as64(Q), _as64(K), _as64(V)
+    B, Hq, Hkv, D = _check_shapes(Q, K, V, L)
+    if dO.shape != Q.shape:
+        raise ValueError("dO must have Q's shape")
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = visibility_mask(L, S)
+    N = 2 * L
+    dQ = np.full(Q.shape, np.nan)
+    dK = np.full(K.shape, np.nan)
+    dV = np.full(V.shape, np.nan)
+    todo = [(b, g) for b in range(B) for g in range(Hkv)] if groups is None else list(groups)
+    for b, g in todo:
+        dK[b, g] = 0.0
+        dV[b, g] = 0.0
+        for h in range(g * G, (g + 1) * G):
+            for r0, r1 in _rows(N, row_chunk):
+                Zc = scale * (Q[b, h, r0:r1] @ K[b, g].T)
+                P, _, _ = _softmax_rows(Zc, M[r0:r1])
+                dOc = dO[b, h, r0:r1]
+                Oc = P @ V[b, g]
+                dP = dOc @ V[b, g].T
+                delta = (dOc * Oc).sum(axis=1, keepdims=True)
+                dS = P * (dP - delta)
+                dQ[b, h, r0:r1] = scale * (dS @ K[b, g])
+                dK[b, g] += scale * (dS.T @ Q[b, h, r0:r1])
+                dV[b, g] += P.T @ dOc
+    return dQ, dK, dV

@@ -1,0 +1,96 @@
+"""Seeded synthetic workloads for block-diffusion attention.
+
+This module only describes shapes and draws random numbers; it holds none of
+the attention arithmetic, so both the HIP library's tests and the CPU oracle
+can take their inputs from it.
+
+The shapes stand in for the paper's training workload (SDAR-8B on math data
+with up to 8k-token sequences, Sections 3.1-3.2 and 4.3), whose data and
+weights are not available: Q/K/V are N(0,1) draws (times 0.5 for the bf16
+shapes), dO is N(0,1), drawn on the host in the fixed order Q, K, V, dO from a
+torch CPU generator, then rounded to nearest-even bf16.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    D: int
+    L: int
+    S: int
+    seed: int
+    dtype: str = "bf16"          # storage type of Q/K/V/dO handed to the library
+    amp: float = 0.5             # Q/K/V ~ N(0,1) * amp
+    k_outlier: float = 0.0       # added to every channel of a fraction of K rows
+    outlier_frac: float = 0.0
+
+    @property
+    def N(self) -> int:          # packed length 2L
+        return 2 * self.L
+
+    def describe(self) -> str:
+        return (f"{self.name}: B={self.B} Hq={self.Hq} Hkv={self.Hkv} D={self.D} "
+                f"L={self.L} S={self.S} {self.dtype}")
+
+
+WORKLOADS = {
+    "tiny": Workload("tiny", 1, 1, 1, 64, 64, 4, seed=0, dtype="fp32", amp=1.0),
+    "small": Workload("small", 4, 16, 4, 64, 1024, 4, seed=1),
+    "8b": Workload("8b", 2, 32, 8, 128, 2048, 4, seed=2),
+    "8b_s8": Workload("8b_s8", 2, 32, 8, 128, 2048, 8, seed=3),
+    "8b_s16": Workload("8b_s16", 2, 32, 8, 128, 2048, 16, seed=4),
+    "8b_s32": Workload("8b_s32", 2, 32, 8, 128, 2048, 32, seed=5),
+    "8b_s64": Workload("8b_s64", 2, 32, 8, 128, 2048, 64, seed=6),
+    "long": Workload("long", 1, 32, 8, 128, 8192, 4, seed=7,
+                     k_outlier=8.0, outlier_frac=0.01),
+}
+
+
+def torch_dtype(name: str) -> torch.dtype:
+    return {"bf16": torch.bfloat16, "fp32": torch.float32}[name]
+
+
+def make_inputs(w: Workload, seed: int | None = None, outlier_mode: str = "rows"):
+    """Return CPU tensors q, k, v, do in the workload's storage dtype.
+
+    outlier_mode: "rows" adds k_outlier to every channel of
+    ceil(outlier_frac * B*Hkv*2L) randomly chosen K rows (both halves);
+    "scalars" adds it to that fraction of individual K entries instead.
+    """
+    g = torch.Generator(device="cpu")
+    g.manual_seed(w.seed if seed is None else seed)
+    N = w.N
+    q = torch.randn((w.B, w.Hq, N, w.D), generator=g) * w.amp
+    k = torch.randn((w.B, w.Hkv, N, w.D), generator=g) * w.amp
+    v = torch.randn((w.B, w.Hkv, N, w.D), generator=g) * w.amp
+    do = torch.randn((w.B, w.Hq, N, w.D), generator=g)
+    if w.k_outlier and w.outlier_frac > 0:
+        if outlier_mode == "rows":
+            rows = k.shape[0] * k.shape[1] * N
+            n = -(-int(round(w.outlier_frac * rows * 1e6)) // 1_000_000)
+            idx = torch.randperm(rows, generator=g)[:n]
+            flat = k.view(rows, w.D)
+            flat[idx] += w.k_outlier
+        elif outlier_mode == "scalars":
+            total = k.numel()
+            n = -(-int(round(w.outlier_frac * total * 1e6)) // 1_000_000)
+            idx = torch.randperm(total, generator=g)[:n]
+            k.view(-1)[idx] += w.k_outlier
+        else:
+            raise ValueError(outlier_mode)
+    dt = torch_dtype(w.dtype)
+    return q.to(dt), k.to(dt), v.to(dt), do.to(dt)
+
+
+def make_random_case(B, Hq, Hkv, D, L, S, seed, dtype="bf16", amp=0.5):
+    """Inputs for an arbitrary shape (parity sweeps and edge cases)."""
+    w = Workload("case", B, Hq, Hkv, D, L, S, seed=seed, dtype=dtype, amp=amp)
+    return make_inputs(w)
