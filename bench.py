@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Benchmark: block-diffusion masked attention, forward + backward, on one MI355X.
+
+One step = bd_attn_fwd + bd_attn_bwd over one batch of the 8B-shaped training
+workload (B=2, Hq=32, Hkv=8, D=128, L=2048 so 4096 packed tokens, S=4, bf16
+N(0,1)*0.5 inputs, dO ~ N(0,1)), inputs resident in HBM.  W untimed warm-up
+steps, then K timed steps bracketed by device synchronisation and HIP events
+on the stream the library runs on.
+
+value  = effective TFLOP/s counting only visible (query, key) pairs:
+         (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
+         visible pair, the FlashAttention convention).
+roofline: the dominant kernel's algorithmic FLOPs per launch over its average
+         duration, from events recorded around every kernel launch of the timed
+         steps, against the bf16 dense MFMA peak.
+cpu_baseline: the fp64 oracle (test infrastructure) timed on the host cores on
+         a bounded sample of the same workload (whole GQA groups).
+
+Prints exactly one JSON line on stdout; details go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 bf16 FLOP/clk x 2.4 GHz (dense)
+METRIC = "effective TFLOP/s (unmasked FLOPs) bd_attn fwd+bwd, 8B shape, % of bf16 peak"
+
+
+def visible_pairs(L: int, S: int) -> int:
+    """Visible (query, key) pairs per (batch, head): sum over blocks of
+    2 s_j (P_j + s_j), s_j the block size and P_j the tokens before it."""
+    S = min(S, L)
+    total, prefix = 0, 0
+    for a in range(0, L, S):
+        s = min(S, L - a)
+        total += 2 * s * (prefix + s)
+        prefix += s
+    return total
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, budget_s: float, max_groups: int):
+    import numpy as np
+    import oracle
+    from paper_2512_22234_amd.workloads import make_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+                      or [1])
+        blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()
+                                if i.get("user_api") == "blas"}))
+    except Exception:  # pragma: no cover
+        threads, blas = len(os.sched_getaffinity(0)), "unknown"
+    q, k, v, do = make_inputs(w)
+    G = w.Hq // w.Hkv
+    groups = [(b, g) for b in range(w.B) for g in range(w.Hkv)]
+    done, t_total = 0, 0.0
+    for b, g in groups[:max_groups]:
+        sl = slice(g * G, (g + 1) * G)
+        Q = q[b:b + 1, sl].double().numpy()
+        K = k[b:b + 1, g:g + 1].double().numpy()
+        V = v[b:b + 1, g:g + 1].double().numpy()
+        dO = do[b:b + 1, sl].double().numpy()
+        t0 = time.perf_counter()
+        oracle.forward(Q, K, V, w.L, w.S)
+        oracle.backward(dO, Q, K, V, w.L, w.S)
+        t_total += time.perf_counter() - t0
+        done += 1
+        log(f"[cpu] oracle group {done}: {t_total:.1f}s cumulative")
+        if t_total >= budget_s:
+            break
+    flops = 14 * w.D * visible_pairs(w.L, w.S) * G * done
+    return {"value": round(flops / t_total / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} GQA group(s) ({G} query heads + 1 KV head each) of the {w.name} workload, "
+                      f"fwd+bwd in fp64 numpy ({blas} BLAS), {t_total:.1f} s; same visible-pair FLOP count"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
+    ap.add_argument("--cpu-max-groups", type=int, default=4)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
+              "the block-diffusion attention path here has no multi-GPU mode.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2512_22234_amd as bd
+    from paper_2512_22234_amd.workloads import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    q, k, v, do = (t.to(dev) for t in make_inputs(w))
+    L, S = w.L, w.S
+    o = torch.empty_like(q)
+    lse = torch.empty((w.B, w.Hq, 2 * L), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    code = bd.BD_ATTN_BF16
+    wsf = torch.empty(bd.bd_attn_workspace_bytes(w.B, L, S, w.Hq, w.Hkv, w.D, code, 0), dtype=torch.uint8,
+                      device=dev)
+    wsb = torch.empty(bd.bd_attn_workspace_bytes(w.B, L, S, w.Hq, w.Hkv, w.D, code, 1), dtype=torch.uint8,
+                      device=dev)
+    fwd_names = bd.bd_attn_stage_names(False, code)
+    bwd_names = bd.bd_attn_stage_names(True, code)
+    nf, nb = len(fwd_names) + 1, len(bwd_names) + 1
+    K = args.steps
+    fwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nf)] for _ in range(K)]
+    bwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nb)] for _ in range(K)]
+    for evs in fwd_marks + bwd_marks:   # create the events before the timed region
+        for e in evs:
+            e.record()
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        if i is None:
+            bd.bd_attn_fwd(q, k, v, L, S, out=o, lse=lse, workspace=wsf)
+            bd.bd_attn_bwd(do, q, k, v, o, lse, L, S, dq=dq, dk=dk, dv=dv, workspace=wsb)
+        else:
+            bd.bd_attn_fwd_marked(q, k, v, L, S, fwd_marks[i], out=o, lse=lse, workspace=wsf)
+            bd.bd_attn_bwd_marked(do, q, k, v, o, lse, L, S, bwd_marks[i], dq=dq, dk=dk, dv=dv, workspace=wsb)
+
+    log(f"[bench] {w.describe()}: warmup {args.warmup}, timed {K} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(K):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / K
+    log(f"[bench] timed region: {ms:.4f} ms/step (events), {wall * 1e3 / K:.4f} ms/step (host clock)")
+
+    # per-kernel durations from the marks
+    per = {}
+    for names, marks in ((fwd_names, fwd_marks), (bwd_names, bwd_marks)):
+        for j, name in enumerate(names):
+            per[name] = sum(m[j].elapsed_time(m[j + 1]) for m in marks) / K
+    t_fwd = sum(per[n] for n in fwd_names)
+    t_bwd = sum(per[n] for n in bwd_names)
+
+    npairs = visible_pairs(L, S) * w.B * w.Hq
+    f_fwd, f_bwd, f_bwd8 = 4 * w.D * npairs, 10 * w.D * npairs, 8 * w.D * npairs
+    tflops = (f_fwd + f_bwd) / (ms * 1e-3) / 1e12
+    # algorithmic FLOPs of each kernel (useful work only; recomputation not counted)
+    alg = {"fwd": 4 * w.D * npairs, "bwd_dkdv": 8 * w.D * npairs, "bwd_dq": 2 * w.D * npairs}
+    kernels = {}
+    for name, t in per.items():
+        entry = {"ms": round(t, 5)}
+        if name in alg:
+            entry["tflops"] = round(alg[name] / (t * 1e-3) / 1e12, 2)
+            entry["frac_of_peak"] = round(entry["tflops"] / PEAK_BF16_TFLOPS, 4)
+        kernels[name] = entry
+    dom = max(alg, key=lambda n: per[n])
+    ach = alg[dom] / (per[dom] * 1e-3) / 1e12
+    log(f"[bench] kernels: {json.dumps(kernels)}")
+    log(f"[bench] fwd {t_fwd:.4f} ms ({f_fwd / t_fwd / 1e9:.1f} TFLOP/s eff), bwd {t_bwd:.4f} ms "
+        f"({f_bwd / t_bwd / 1e9:.1f} TFLOP/s eff at 10D, {f_bwd8 / t_bwd / 1e9:.1f} at 8D)")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_budget, args.cpu_max_groups)
+
+    out = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 3),
+        "config": {"workload": f"{w.name}: B={w.B} Hq={w.Hq} Hkv={w.Hkv} D={w.D} L={L} (packed {2 * L}) "
+                               f"S={S}, bf16 N(0,1)*0.5, fwd+bwd",
+                   "global_batch": w.B, "seq_len": 2 * L, "parallelism": "single GPU",
+                   "visible_pairs_per_head": visible_pairs(L, S),
+                   "flops_per_step": f_fwd + f_bwd, "fwd_ms": round(t_fwd, 5), "bwd_ms": round(t_bwd, 5)},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

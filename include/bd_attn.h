@@ -1,0 +1,150 @@
+/*
+ * bd_attn — block-diffusion masked attention (forward and backward) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (DiRL, arXiv 2512.22234, Section 4.1 with the block rules of
+ * Section 2.1, Eq. 1 and Eq. 2): attention over a packed sequence of 2L
+ * tokens [x_t | x_0], the noisy copy first.  With the block index
+ * b(p) = (p mod L) div S of packed position p:
+ *   - a noisy query (p < L) sees noisy keys of its own block (both
+ *     directions) and clean keys of strictly earlier blocks;
+ *   - a clean query sees clean keys of its own and earlier blocks and never
+ *     a noisy key.
+ * O = softmax(scale * Q K^T restricted to visible keys) V, per query head h,
+ * using KV head h div (Hq / Hkv).
+ *
+ * Layouts (all contiguous, innermost dimension last, 16-byte aligned):
+ *   Q, O, dO, dQ : [B, Hq,  2L, D]
+ *   K, V, dK, dV : [B, Hkv, 2L, D]
+ *   LSE          : [B, Hq,  2L] float32 (4-byte aligned), natural-log
+ *                  log-sum-exp of the scaled scores of each row over its
+ *                  visible keys.
+ * Element type of Q/K/V/O/dO/dQ/dK/dV is selected by `dtype`:
+ *   BD_ATTN_BF16 (0): bfloat16 — the compute path;
+ *   BD_ATTN_FP32 (1): float32, rounded to bfloat16 inside the library (the
+ *                     arithmetic is the bf16 path) and written back as float32.
+ * D must be 64 or 128.  S >= L behaves as S = L.  S need not divide L (the
+ * last block is then shorter).  scale <= 0 selects 1/sqrt(D).
+ *
+ * Ownership and ordering: the caller allocates every buffer, including the
+ * workspace (size from bd_attn_workspace_bytes, at least 16-byte aligned).  The
+ * library never allocates, frees or synchronises; all work is enqueued on
+ * `stream` in order and the call returns without waiting.  Outputs must not
+ * overlap inputs.  The workspace may be reused once the enqueued work has
+ * completed (stream order guarantees this for calls on the same stream).
+ * The library keeps no mutable global state; calls from several host threads
+ * are safe.
+ *
+ * Errors: every entry point validates its arguments before enqueuing
+ * anything; a call that returns non-zero has enqueued no work (except
+ * BD_ATTN_ERR_HIP, reported from the launch itself).  No C++ exception
+ * crosses this interface.
+ */
+#ifndef BD_ATTN_H
+#define BD_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum bd_attn_status {
+  BD_ATTN_OK = 0,
+  BD_ATTN_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, B,L,S<1, Hq%Hkv!=0, overlap */
+  BD_ATTN_ERR_UNSUPPORTED = 2,      /* D not in {64,128}, unknown dtype */
+  BD_ATTN_ERR_WORKSPACE_TOO_SMALL = 3,
+  BD_ATTN_ERR_HIP = 4               /* a HIP launch reported an error */
+};
+
+enum bd_attn_dtype { BD_ATTN_BF16 = 0, BD_ATTN_FP32 = 1 };
+
+/* Tile classes returned by bd_attn_classify_tiles_host. */
+enum bd_attn_tile_class { BD_TILE_EMPTY = 0, BD_TILE_FULL = 1, BD_TILE_PARTIAL = 2 };
+
+/*
+ * Forward pass (Section 4.1; masking rules of Eq. 1 and Eq. 2).
+ * Inputs Q, K, V; outputs O (same dtype as the inputs) and LSE (float32).
+ * ws/ws_bytes: device workspace of at least
+ * bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, dtype, 0) bytes.
+ */
+int bd_attn_fwd(const void* Q, const void* K, const void* V,
+                int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward pass: the vector-Jacobian product of the forward pass for the
+ * upstream gradient dO, given the forward's O and LSE.  Writes dQ, dK, dV
+ * (dK and dV summed over the Hq/Hkv query heads sharing each KV head).
+ * Deterministic: no atomics, results are bitwise reproducible.
+ * ws/ws_bytes: at least bd_attn_workspace_bytes(..., for_bwd = 1) bytes.
+ */
+int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
+                const void* O, const float* LSE,
+                int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Workspace bytes needed by bd_attn_fwd (for_bwd = 0) or bd_attn_bwd
+ * (for_bwd = 1).  Returns 0 for arguments the calls would reject.
+ */
+size_t bd_attn_workspace_bytes(int B, int L, int S, int Hq, int Hkv, int D, int dtype, int for_bwd);
+
+/*
+ * Host-side copy of the tile classifier the kernels use (exposed for tests).
+ * Tiles are half-local: each half of the packed sequence is cut into
+ * ceil(L/BM) query tiles and ceil(L/BN) key tiles, the last one shorter when
+ * L is not a multiple; no tile straddles position L.  Writes one class per
+ * (query tile, key tile) pair, row-major, into out[nq * nk] with
+ * nq = 2*ceil(L/BM), nk = 2*ceil(L/BN) (query tiles and key tiles numbered
+ * noisy half first).  EMPTY: no visible pair; FULL: every pair visible and
+ * both tiles full-sized; PARTIAL otherwise.  Returns a status.
+ */
+int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
+
+/*
+ * Host-side copy of the tile walk the kernels perform (exposed for tests).
+ * Same tiling and out[] indexing as bd_attn_classify_tiles_host; writes, per
+ * (query tile, key tile) pair, how many times the kernels visit it: walking
+ * key tiles per query tile (forward and dQ, by_key_tile = 0) or query tiles
+ * per key tile (dK/dV, by_key_tile = 1; that kernel repeats the walk for each
+ * query head of the group).  A correct walk visits every non-EMPTY pair
+ * exactly once.
+ */
+int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out);
+
+/*
+ * Benchmark variants of bd_attn_fwd / bd_attn_bwd: identical work and
+ * validation, and in addition hipEventRecord(marks[i], stream) for caller-
+ * created events: marks[0] before the first kernel launch and marks[i] right
+ * after launch i, for as many marks as n_marks allows.  The kernels launched,
+ * in order, are named by bd_attn_stage_names.  Intended for measuring each
+ * kernel's duration on the stream it runs on.
+ */
+int bd_attn_fwd_marked(const void* Q, const void* K, const void* V,
+                       int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                       void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream,
+                       hipEvent_t* marks, int n_marks);
+int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void* V,
+                       const void* O, const float* LSE,
+                       int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                       void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream,
+                       hipEvent_t* marks, int n_marks);
+
+/* Comma-separated names of the kernels bd_attn_fwd (for_bwd = 0) or
+ * bd_attn_bwd (for_bwd = 1) launch for `dtype`, in launch order (static). */
+const char* bd_attn_stage_names(int for_bwd, int dtype);
+
+/* Static, human-readable text for a status code. */
+const char* bd_attn_status_string(int status);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int bd_attn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BD_ATTN_H */

@@ -11,4 +11,5 @@ from .bd_attn_oracle import (  # noqa: F401
     forward,
     backward,
     probabilities,
+    sampled,
 )

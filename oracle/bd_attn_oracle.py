@@ -181,3 +181,48 @@ def backward(dO, Q, K, V, L: int, S: int, scale: float | None = None,
                 dK[b, g] += scale * (dS.T @ Q[b, h, r0:r1])
                 dV[b, g] += P.T @ dOc
     return dQ, dK, dV
+
+
+def sampled(dO, Q, K, V, L: int, S: int, b: int, hkv: int, query_rows, key_rows,
+            scale: float | None = None, row_chunk: int = 1024):
+    """Selected outputs of one KV group (batch b, KV head hkv), for shapes too
+    large to evaluate whole.
+
+    For every query head h of the group: O, LSE and dQ at `query_rows`.
+    For the KV head: dK and dV at `key_rows`, summed over the group's query
+    heads and over every query that sees those keys (queries that see none of
+    them contribute exactly zero, since P vanishes there).  Each needed query
+    row is evaluated in full with the same definitions as forward/backward.
+    Returns dict with O [G,nq,D], LSE [G,nq], dQ [G,nq,D], dK [nk,D], dV [nk,D].
+    """
+    Qb, Kb, Vb, dOb = _as64(Q[b]), _as64(K[b, hkv]), _as64(V[b, hkv]), _as64(dO[b])
+    Hq, N, D = Qb.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = visibility_mask(L, S)
+    qr = np.asarray(list(query_rows), dtype=np.int64)
+    kr = np.asarray(list(key_rows), dtype=np.int64)
+    seers = np.nonzero(M[:, kr].any(axis=1))[0] if len(kr) else np.zeros(0, np.int64)
+    out = {"O": np.zeros((G, len(qr), D)), "LSE": np.zeros((G, len(qr))),
+           "dQ": np.zeros((G, len(qr), D)), "dK": np.zeros((len(kr), D)), "dV": np.zeros((len(kr), D))}
+    for gi in range(G):
+        h = hkv * G + gi
+        for rows, is_query in ((qr, True), (seers, False)):
+            for r0, r1 in _rows(len(rows), row_chunk):
+                idx = rows[r0:r1]
+                Zc = scale * (Qb[h, idx] @ Kb.T)
+                P, m, l = _softmax_rows(Zc, M[idx])
+                Oc = P @ Vb
+                dOc = dOb[h, idx]
+                dP = dOc @ Vb.T
+                delta = (dOc * Oc).sum(axis=1, keepdims=True)
+                dS = P * (dP - delta)
+                if is_query:
+                    out["O"][gi, r0:r1] = Oc
+                    out["LSE"][gi, r0:r1] = (m + np.log(l))[:, 0]
+                    out["dQ"][gi, r0:r1] = scale * (dS @ Kb)
+                else:
+                    out["dK"] += scale * (dS[:, kr].T @ Qb[h, idx])
+                    out["dV"] += P[:, kr].T @ dOc
+    return out

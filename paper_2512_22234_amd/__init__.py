@@ -1,0 +1,209 @@
+"""bd_attn: block-diffusion masked attention for MI355X (gfx950).
+
+Thin Python binding over the C-ABI library libbd_attn.so: the functions here
+carry the names of the C entry points and only marshal arguments (shape and
+dtype checks, output/workspace allocation through torch, the current HIP
+stream).  Every step of the computation runs in the library's HIP kernels.
+
+Attention over the packed sequence [x_t | x_0] of 2L tokens with the
+block-diffusion mask of DiRL (arXiv 2512.22234, Section 4.1; Eq. 1 and
+Eq. 2): a noisy query sees noisy keys of its own block and clean keys of
+earlier blocks; a clean query sees clean keys of its own and earlier blocks.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from ._lib import LIB_PATH, BdAttnError, lib, status_string  # noqa: F401
+
+BD_ATTN_BF16 = 0
+BD_ATTN_FP32 = 1
+
+__all__ = [
+    "bd_attn", "BdAttnFunction", "bd_attn_fwd", "bd_attn_bwd", "bd_attn_workspace_bytes",
+    "bd_attn_classify_tiles_host", "bd_attn_visit_lists_host", "bd_attn_status_string",
+    "bd_attn_version", "bd_attn_fwd_marked", "bd_attn_bwd_marked", "bd_attn_stage_names",
+    "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
+]
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BD_ATTN_BF16
+    if t.dtype == torch.float32:
+        return BD_ATTN_FP32
+    raise TypeError(f"bd_attn supports bfloat16 and float32 tensors, got {t.dtype}")
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device, stream):
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return s, ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(name: str, t: torch.Tensor, shape, dtype, device):
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name}: expected device {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+
+
+def _scale_arg(scale) -> float:
+    return 0.0 if scale is None else float(scale)
+
+
+def bd_attn_version() -> int:
+    return int(lib().bd_attn_version())
+
+
+def bd_attn_status_string(status: int) -> str:
+    return status_string(status)
+
+
+def bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, dtype, for_bwd) -> int:
+    return int(lib().bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, int(dtype), int(for_bwd)))
+
+
+def bd_attn_classify_tiles_host(L: int, S: int, BM: int, BN: int) -> np.ndarray:
+    nq, nk = 2 * (-(-L // BM)), 2 * (-(-L // BN))
+    out = np.zeros((nq, nk), dtype=np.int8)
+    st = lib().bd_attn_classify_tiles_host(L, S, BM, BN, out.ctypes.data_as(ctypes.c_void_p))
+    if st:
+        raise BdAttnError(st, "bd_attn_classify_tiles_host")
+    return out
+
+
+def bd_attn_visit_lists_host(L: int, S: int, BM: int, BN: int, by_key_tile: bool) -> np.ndarray:
+    nq, nk = 2 * (-(-L // BM)), 2 * (-(-L // BN))
+    out = np.zeros((nq, nk), dtype=np.int8)
+    st = lib().bd_attn_visit_lists_host(L, S, BM, BN, int(by_key_tile), out.ctypes.data_as(ctypes.c_void_p))
+    if st:
+        raise BdAttnError(st, "bd_attn_visit_lists_host")
+    return out
+
+
+def _shapes(q, k, L):
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("q [B,Hq,2L,D] and k/v [B,Hkv,2L,D] expected")
+    B, Hq, N, D = q.shape
+    Hkv = k.shape[1]
+    if N != 2 * L:
+        raise ValueError(f"packed length {N} != 2L = {2 * L}")
+    return B, Hq, Hkv, D
+
+
+def _marks_arg(marks):
+    """ctypes array of raw HIP event handles from torch.cuda.Event objects."""
+    if not marks:
+        return None, 0
+    for ev in marks:
+        if ev.cuda_event == 0:      # torch creates the event lazily on first record
+            ev.record()
+    arr = (ctypes.c_void_p * len(marks))(*[ev.cuda_event for ev in marks])
+    return arr, len(marks)
+
+
+def bd_attn_stage_names(for_bwd: bool, dtype: int = BD_ATTN_BF16):
+    return lib().bd_attn_stage_names(int(for_bwd), int(dtype)).decode().split(",")
+
+
+def bd_attn_fwd_marked(q, k, v, L: int, S: int, marks, scale=None, out=None, lse=None, workspace=None,
+                       stream=None):
+    """bd_attn_fwd that also records marks[0] before and marks[i] after kernel i."""
+    return bd_attn_fwd(q, k, v, L, S, scale, out, lse, workspace, stream, _marks=marks)
+
+
+def bd_attn_bwd_marked(do, q, k, v, o, lse, L: int, S: int, marks, scale=None, dq=None, dk=None, dv=None,
+                       workspace=None, stream=None):
+    """bd_attn_bwd that also records marks[0] before and marks[i] after kernel i."""
+    return bd_attn_bwd(do, q, k, v, o, lse, L, S, scale, dq, dk, dv, workspace, stream, _marks=marks)
+
+
+def bd_attn_fwd(q, k, v, L: int, S: int, scale=None, out=None, lse=None, workspace=None, stream=None,
+                _marks=None):
+    """Forward pass; returns (O, LSE).  O has q's dtype, LSE is float32 [B,Hq,2L]."""
+    B, Hq, Hkv, D = _shapes(q, k, L)
+    dev, dt = q.device, q.dtype
+    code = _dtype_code(q)
+    _check("q", q, (B, Hq, 2 * L, D), dt, dev)
+    _check("k", k, (B, Hkv, 2 * L, D), dt, dev)
+    _check("v", v, (B, Hkv, 2 * L, D), dt, dev)
+    o = torch.empty_like(q) if out is None else out
+    l_ = torch.empty((B, Hq, 2 * L), dtype=torch.float32, device=dev) if lse is None else lse
+    _check("out", o, q.shape, dt, dev)
+    _check("lse", l_, (B, Hq, 2 * L), torch.float32, dev)
+    nbytes = bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, code, 0)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    args = (_ptr(q), _ptr(k), _ptr(v), B, L, S, Hq, Hkv, D, _scale_arg(scale), code,
+            _ptr(o), _ptr(l_), _ptr(ws), ws.numel(), sh)
+    if _marks:
+        st = lib().bd_attn_fwd_marked(*args, *_marks_arg(_marks))
+    else:
+        st = lib().bd_attn_fwd(*args)
+    if st:
+        raise BdAttnError(st, "bd_attn_fwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return o, l_
+
+
+def bd_attn_bwd(do, q, k, v, o, lse, L: int, S: int, scale=None, dq=None, dk=None, dv=None,
+                workspace=None, stream=None, _marks=None):
+    """Backward pass; returns (dQ, dK, dV) in q's dtype."""
+    B, Hq, Hkv, D = _shapes(q, k, L)
+    dev, dt = q.device, q.dtype
+    code = _dtype_code(q)
+    for name, t, shp in (("do", do, q.shape), ("q", q, q.shape), ("k", k, (B, Hkv, 2 * L, D)),
+                         ("v", v, (B, Hkv, 2 * L, D)), ("o", o, q.shape)):
+        _check(name, t, shp, dt, dev)
+    _check("lse", lse, (B, Hq, 2 * L), torch.float32, dev)
+    dq_ = torch.empty_like(q) if dq is None else dq
+    dk_ = torch.empty_like(k) if dk is None else dk
+    dv_ = torch.empty_like(v) if dv is None else dv
+    nbytes = bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, code, 1)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    args = (_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, S, Hq, Hkv, D,
+            _scale_arg(scale), code, _ptr(dq_), _ptr(dk_), _ptr(dv_), _ptr(ws), ws.numel(), sh)
+    if _marks:
+        st = lib().bd_attn_bwd_marked(*args, *_marks_arg(_marks))
+    else:
+        st = lib().bd_attn_bwd(*args)
+    if st:
+        raise BdAttnError(st, "bd_attn_bwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return dq_, dk_, dv_
+
+
+class BdAttnFunction(torch.autograd.Function):
+    """Autograd wrapper: forward saves Q, K, V, O, LSE; backward returns dQ, dK, dV."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, L, S, scale=None):
+        o, lse = bd_attn_fwd(q, k, v, L, S, scale)
+        ctx.save_for_backward(q, k, v, o, lse)
+        ctx.L, ctx.S, ctx.scale = L, S, scale
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        q, k, v, o, lse = ctx.saved_tensors
+        dq, dk, dv = bd_attn_bwd(do.contiguous(), q, k, v, o, lse, ctx.L, ctx.S, ctx.scale)
+        return dq, dk, dv, None, None, None
+
+
+def bd_attn(q, k, v, L: int, S: int, scale=None):
+    """Block-diffusion masked attention over [x_t | x_0]; differentiable."""
+    return BdAttnFunction.apply(q, k, v, L, S, scale)

@@ -1,0 +1,324 @@
+// C-ABI entry points: argument validation, workspace layout, launch sequence.
+// No exception crosses this boundary; nothing is enqueued unless every
+// argument checks out.
+#include <stdint.h>
+#include <string.h>
+
+#include <cmath>
+
+#include "../../include/bd_attn.h"
+#include "kernels.hpp"
+#include "tiles.hpp"
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t kvt = 0, delta = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
+};
+
+bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
+  return B >= 1 && L >= 1 && S >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 && L <= (1 << 28);
+}
+
+Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
+  Layout w;
+  const size_t N = 2 * (size_t)L;
+  const size_t Lp = (size_t)bd::cdiv(L, bd::KEY_PAD) * bd::KEY_PAD;
+  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  size_t off = 0;
+  w.kvt = off;
+  off += align256((size_t)B * Hkv * D * 2 * Lp * 2);
+  if (bwd) {
+    w.delta = off;
+    off += align256((size_t)B * Hq * N * 4);
+  }
+  if (dtype == BD_ATTN_FP32) {
+    w.q = off; off += align256(nq * 2);
+    w.k = off; off += align256(nk * 2);
+    w.v = off; off += align256(nk * 2);
+    w.o = off; off += align256(nq * 2);
+    if (bwd) {
+      w.dout = off; off += align256(nq * 2);
+      w.dq = off; off += align256(nq * 2);
+      w.dk = off; off += align256(nk * 2);
+      w.dv = off; off += align256(nk * 2);
+    }
+  }
+  w.total = off;
+  return w;
+}
+
+struct Range {
+  const void* p;
+  size_t n;
+};
+
+bool overlap(const Range& a, const Range& b) {
+  const uintptr_t a0 = (uintptr_t)a.p, b0 = (uintptr_t)b.p;
+  return a0 < b0 + b.n && b0 < a0 + a.n;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Common validation; fills the resolved shape.
+int validate(int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, bd::Shape& s) {
+  if (!shape_ok(B, L, S, Hq, Hkv)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (D != 64 && D != 128) return BD_ATTN_ERR_UNSUPPORTED;
+  if (dtype != BD_ATTN_BF16 && dtype != BD_ATTN_FP32) return BD_ATTN_ERR_UNSUPPORTED;
+  s.B = B;
+  s.L = L;
+  s.S = S > L ? L : S;
+  s.Hq = Hq;
+  s.Hkv = Hkv;
+  s.D = D;
+  s.G = Hq / Hkv;
+  s.Lp = bd::cdiv(L, bd::KEY_PAD) * bd::KEY_PAD;
+  s.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)D);
+  return BD_ATTN_OK;
+}
+
+#define BD_TRY(expr)                                    \
+  do {                                                  \
+    if ((expr) != hipSuccess) return BD_ATTN_ERR_HIP;   \
+  } while (0)
+
+#define BD_LAUNCH(expr)                                                     \
+  do {                                                                      \
+    if ((expr) != hipSuccess || marks.rec(stream) != hipSuccess) return BD_ATTN_ERR_HIP; \
+  } while (0)
+
+// Optional caller-owned events recorded on the stream: mark 0 before the first
+// launch, mark i after launch i (benchmark entry points only).
+struct Marks {
+  hipEvent_t* ev;
+  int n;
+  int i = 0;
+  hipError_t rec(hipStream_t st) {
+    if (ev == nullptr || i >= n) return hipSuccess;
+    return hipEventRecord(ev[i++], st);
+  }
+};
+
+int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
+             float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream,
+             Marks marks);
+int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
+             int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
+             void* dV, void* ws, size_t ws_bytes, hipStream_t stream, Marks marks);
+
+}  // namespace
+
+extern "C" {
+
+int bd_attn_version(void) { return kVersion; }
+
+const char* bd_attn_status_string(int status) {
+  switch (status) {
+    case BD_ATTN_OK: return "ok";
+    case BD_ATTN_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case BD_ATTN_ERR_UNSUPPORTED: return "unsupported head dimension or dtype";
+    case BD_ATTN_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case BD_ATTN_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+size_t bd_attn_workspace_bytes(int B, int L, int S, int Hq, int Hkv, int D, int dtype, int for_bwd) {
+  bd::Shape s;
+  if (validate(B, L, S, Hq, Hkv, D, 0.f, dtype, s) != BD_ATTN_OK) return 0;
+  return make_layout(B, L, Hq, Hkv, D, dtype, for_bwd != 0).total;
+}
+
+int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out) {
+  if (L < 1 || S < 1 || BM < 1 || BN < 1 || out == nullptr) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (S > L) S = L;
+  const int nqt = bd::cdiv(L, BM), nkt = bd::cdiv(L, BN);
+  const int nq = 2 * nqt, nk = 2 * nkt;
+  for (int a = 0; a < nq; ++a) {
+    const int qh = a / nqt, i = a % nqt;
+    const int q0 = i * BM, q1 = bd::imin(L, q0 + BM);
+    for (int c = 0; c < nk; ++c) {
+      const int kh = c / nkt, j = c % nkt;
+      const int k0 = j * BN, k1 = bd::imin(L, k0 + BN);
+      out[(size_t)a * nk + c] =
+          (int8_t)bd::classify_pair(qh, q0, q1, kh, k0, k1, S, (q1 - q0) == BM && (k1 - k0) == BN);
+    }
+  }
+  return BD_ATTN_OK;
+}
+
+int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out) {
+  if (L < 1 || S < 1 || BM < 1 || BN < 1 || out == nullptr) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (S > L) S = L;
+  const int nqt = bd::cdiv(L, BM), nkt = bd::cdiv(L, BN);
+  const int nq = 2 * nqt, nk = 2 * nkt;
+  memset(out, 0, (size_t)nq * nk);
+  if (!by_key_tile) {
+    for (int a = 0; a < nq; ++a) {
+      const bd::KeyTileList kl = bd::key_tiles_for_query_tile(a / nqt, a % nqt, L, S, BM, BN);
+      for (int t = 0; t < kl.count(); ++t) {
+        int kh, j;
+        kl.at(t, kh, j);
+        if (j < 0 || j >= nkt) return BD_ATTN_ERR_INVALID_ARGUMENT;
+        out[(size_t)a * nk + kh * nkt + j] += 1;
+      }
+    }
+  } else {
+    for (int c = 0; c < nk; ++c) {
+      const bd::QueryTileList ql = bd::query_tiles_for_key_tile(c / nkt, c % nkt, L, S, BM, BN);
+      for (int t = 0; t < ql.count(); ++t) {
+        int qh, i;
+        ql.at(t, qh, i);
+        if (i < 0 || i >= nqt) return BD_ATTN_ERR_INVALID_ARGUMENT;
+        out[(size_t)(qh * nqt + i) * nk + c] += 1;
+      }
+    }
+  }
+  return BD_ATTN_OK;
+}
+
+int bd_attn_fwd(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
+                float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return fwd_impl(Q, K, V, B, L, S, Hq, Hkv, D, scale, dtype, O, LSE, ws, ws_bytes, stream, Marks{nullptr, 0});
+}
+
+int bd_attn_fwd_marked(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv,
+                       int D, float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes,
+                       hipStream_t stream, hipEvent_t* marks, int n_marks) {
+  return fwd_impl(Q, K, V, B, L, S, Hq, Hkv, D, scale, dtype, O, LSE, ws, ws_bytes, stream,
+                  Marks{marks, n_marks});
+}
+
+int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
+                int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
+                void* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return bwd_impl(dO, Q, K, V, O, LSE, B, L, S, Hq, Hkv, D, scale, dtype, dQ, dK, dV, ws, ws_bytes, stream,
+                  Marks{nullptr, 0});
+}
+
+int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                       const float* LSE, int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                       void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream,
+                       hipEvent_t* marks, int n_marks) {
+  return bwd_impl(dO, Q, K, V, O, LSE, B, L, S, Hq, Hkv, D, scale, dtype, dQ, dK, dV, ws, ws_bytes, stream,
+                  Marks{marks, n_marks});
+}
+
+const char* bd_attn_stage_names(int for_bwd, int dtype) {
+  if (dtype == BD_ATTN_FP32)
+    return for_bwd ? "cast_q,cast_k,cast_v,cast_o,cast_do,bwd_pre,transpose_k,bwd_dkdv,bwd_dq,cast_dq,cast_dk,cast_dv"
+                   : "cast_q,cast_k,cast_v,transpose_v,fwd,cast_o";
+  return for_bwd ? "bwd_pre,transpose_k,bwd_dkdv,bwd_dq" : "transpose_v,fwd";
+}
+
+}  // extern "C"
+
+namespace {
+
+int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
+             float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream,
+             Marks marks) {
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  if (!Q || !K || !V || !O || !LSE || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4) ||
+      !aligned(ws, 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
+  const size_t N = 2 * (size_t)L;
+  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, false);
+  const Range in[] = {{Q, nq * esz}, {K, nk * esz}, {V, nk * esz}};
+  const Range out[] = {{O, nq * esz}, {LSE, (size_t)B * Hq * N * 4}, {ws, w.total}};
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2]))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
+
+  (void)hipGetLastError();  // clear a stale error so it is not reported as ours
+  BD_TRY(marks.rec(stream));
+  char* wb = static_cast<char*>(ws);
+  const void *q = Q, *k = K, *v = V;
+  void* o = O;
+  if (dtype == BD_ATTN_FP32) {
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream));
+    q = wb + w.q;
+    k = wb + w.k;
+    v = wb + w.v;
+    o = wb + w.o;
+  }
+  BD_LAUNCH(bd::launch_transpose_keys(v, wb + w.kvt, B * Hkv, L, s.Lp, D, stream));
+  BD_LAUNCH(bd::launch_fwd(s, q, k, wb + w.kvt, o, LSE, stream));
+  if (dtype == BD_ATTN_FP32) BD_LAUNCH(bd::launch_cast_bf16_to_f32(o, static_cast<float*>(O), nq, stream));
+  return BD_ATTN_OK;
+}
+
+int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
+             int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
+             void* dV, void* ws, size_t ws_bytes, hipStream_t stream, Marks marks) {
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  if (!dO || !Q || !K || !V || !O || !LSE || !dQ || !dK || !dV || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!aligned(dO, 16) || !aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+      !aligned(LSE, 4) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) || !aligned(ws, 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
+  const size_t N = 2 * (size_t)L;
+  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, true);
+  const Range in[] = {{dO, nq * esz}, {Q, nq * esz}, {K, nk * esz}, {V, nk * esz}, {O, nq * esz},
+                      {LSE, (size_t)B * Hq * N * 4}};
+  const Range out[] = {{dQ, nq * esz}, {dK, nk * esz}, {dV, nk * esz}, {ws, w.total}};
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  for (int a = 0; a < 4; ++a)
+    for (int c = a + 1; c < 4; ++c)
+      if (overlap(out[a], out[c])) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
+
+  (void)hipGetLastError();
+  BD_TRY(marks.rec(stream));
+  char* wb = static_cast<char*>(ws);
+  const void *q = Q, *k = K, *v = V, *o = O, *g = dO;
+  void *dq = dQ, *dk = dK, *dv = dV;
+  if (dtype == BD_ATTN_FP32) {
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(O), wb + w.o, nq, stream));
+    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(dO), wb + w.dout, nq, stream));
+    q = wb + w.q;
+    k = wb + w.k;
+    v = wb + w.v;
+    o = wb + w.o;
+    g = wb + w.dout;
+    dq = wb + w.dq;
+    dk = wb + w.dk;
+    dv = wb + w.dv;
+  }
+  float* delta = reinterpret_cast<float*>(wb + w.delta);
+  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, delta, stream));
+  BD_LAUNCH(bd::launch_transpose_keys(k, wb + w.kvt, B * Hkv, L, s.Lp, D, stream));
+  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, LSE, delta, dk, dv, stream));
+  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, wb + w.kvt, v, g, LSE, delta, dq, stream));
+  if (dtype == BD_ATTN_FP32) {
+    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
+    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));
+    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dv, static_cast<float*>(dV), nk, stream));
+  }
+  return BD_ATTN_OK;
+}
+
+}  // namespace

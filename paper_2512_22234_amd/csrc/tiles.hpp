@@ -1,0 +1,135 @@
+// Tile geometry and exact tile classification for the block-diffusion mask.
+//
+// Packed sequence [x_t | x_0] of 2L positions; each half is cut into tiles
+// independently ("half-local" tiles, the last one shorter when the tile size
+// does not divide L), so every tile lies in one half and the quadrant of a
+// (query tile, key tile) pair is fixed.  Inside a half the block index
+// b = local_position div S is non-decreasing, so the block-index range of a
+// tile is [first div S, last div S] and the class of a pair follows from the
+// two ranges alone (DiRL Section 4.1 with the rules of Eq. 1 and Eq. 2):
+//
+//   quadrant      visible pair when     FULL iff            EMPTY iff
+//   noisy-noisy   bk == bq              qlo=qhi=klo=khi     qhi<klo or khi<qlo
+//   noisy-clean   bk <  bq              khi <  qlo          klo >= qhi
+//   clean-clean   bk <= bq              khi <= qlo          klo >  qhi
+//   clean-noisy   never                 never               always
+//
+// A pair that is not EMPTY is downgraded from FULL to PARTIAL when either tile
+// is short (ragged end of a half), so that a FULL tile can run with no
+// per-element test at all.
+//
+// This header is plain C++ apart from the host/device qualifiers, so the host
+// classifier exported by the library and the kernels use the same code.
+#pragma once
+
+#ifdef __HIPCC__
+#define BD_HD __host__ __device__ inline
+#else
+#define BD_HD inline
+#endif
+
+namespace bd {
+
+enum { TILE_EMPTY = 0, TILE_FULL = 1, TILE_PARTIAL = 2 };
+enum { HALF_NOISY = 0, HALF_CLEAN = 1 };
+
+BD_HD int cdiv(int a, int b) { return (a + b - 1) / b; }
+BD_HD int imin(int a, int b) { return a < b ? a : b; }
+BD_HD int imax(int a, int b) { return a > b ? a : b; }
+
+// Is key (half kh, block bk) visible from query (half qh, block bq)?
+BD_HD bool visible(int qh, int bq, int kh, int bk) {
+  if (qh == HALF_NOISY) return kh == HALF_NOISY ? bk == bq : bk < bq;
+  return kh == HALF_CLEAN && bk <= bq;
+}
+
+// Class of the pair (query rows [q0,q1) of half qh, keys [k0,k1) of half kh);
+// local indices, both ranges non-empty.  full_size: both tiles full-sized.
+BD_HD int classify_pair(int qh, int q0, int q1, int kh, int k0, int k1, int S, bool full_size) {
+  const int qlo = q0 / S, qhi = (q1 - 1) / S, klo = k0 / S, khi = (k1 - 1) / S;
+  int cls;
+  if (qh == HALF_NOISY && kh == HALF_NOISY) {
+    if (qhi < klo || khi < qlo) return TILE_EMPTY;
+    cls = (qlo == qhi && klo == khi && qlo == klo) ? TILE_FULL : TILE_PARTIAL;
+  } else if (qh == HALF_NOISY) {
+    if (klo >= qhi) return TILE_EMPTY;
+    cls = (khi < qlo) ? TILE_FULL : TILE_PARTIAL;
+  } else if (kh == HALF_CLEAN) {
+    if (klo > qhi) return TILE_EMPTY;
+    cls = (khi <= qlo) ? TILE_FULL : TILE_PARTIAL;
+  } else {
+    return TILE_EMPTY;
+  }
+  if (cls == TILE_FULL && !full_size) cls = TILE_PARTIAL;
+  return cls;
+}
+
+// Key tiles visited by query tile (qh, i): clean key tiles [0, nclean) then,
+// for a noisy query tile, noisy key tiles [noisy0, noisy0 + nnoisy).
+struct KeyTileList {
+  int nclean, noisy0, nnoisy;
+  BD_HD int count() const { return nclean + nnoisy; }
+  // t-th visited key tile: half and index
+  BD_HD void at(int t, int& kh, int& j) const {
+    if (t < nclean) { kh = HALF_CLEAN; j = t; }
+    else { kh = HALF_NOISY; j = noisy0 + (t - nclean); }
+  }
+};
+
+BD_HD KeyTileList key_tiles_for_query_tile(int qh, int i, int L, int S, int BM, int BN) {
+  const int nKT = cdiv(L, BN);
+  const int q0 = i * BM, q1 = imin(L, q0 + BM);
+  const int qlo = q0 / S, qhi = (q1 - 1) / S;
+  KeyTileList r;
+  if (qh == HALF_NOISY) {
+    // clean key tile j is visible iff its first block < qhi, i.e. j*BN < qhi*S
+    r.nclean = imin(nKT, cdiv(qhi * S, BN));
+    // noisy keys whose block lies in [qlo, qhi]
+    const int kfirst = qlo * S, klast = imin(L, (qhi + 1) * S) - 1;
+    r.noisy0 = kfirst / BN;
+    r.nnoisy = klast / BN - r.noisy0 + 1;
+  } else {
+    // clean key tile j is visible iff its first block <= qhi
+    r.nclean = imin(nKT, cdiv((qhi + 1) * S, BN));
+    r.noisy0 = 0;
+    r.nnoisy = 0;
+  }
+  return r;
+}
+
+// Query tiles visited by key tile (kh, j): noisy query tiles
+// [noisy0, noisy0 + nnoisy) then clean query tiles [clean0, clean0 + nclean).
+struct QueryTileList {
+  int noisy0, nnoisy, clean0, nclean;
+  BD_HD int count() const { return nnoisy + nclean; }
+  BD_HD void at(int t, int& qh, int& i) const {
+    if (t < nnoisy) { qh = HALF_NOISY; i = noisy0 + t; }
+    else { qh = HALF_CLEAN; i = clean0 + (t - nnoisy); }
+  }
+};
+
+BD_HD QueryTileList query_tiles_for_key_tile(int kh, int j, int L, int S, int BM, int BN) {
+  const int nQT = cdiv(L, BM);
+  const int k0 = j * BN, k1 = imin(L, k0 + BN);
+  const int klo = k0 / S, khi = (k1 - 1) / S;
+  QueryTileList r;
+  if (kh == HALF_NOISY) {
+    // noisy queries whose block lies in [klo, khi]
+    const int qfirst = klo * S, qlast = imin(L, (khi + 1) * S) - 1;
+    r.noisy0 = qfirst / BM;
+    r.nnoisy = qlast / BM - r.noisy0 + 1;
+    r.clean0 = 0;
+    r.nclean = 0;
+  } else {
+    // noisy queries with block > klo start at row (klo+1)*S
+    const int qn = (klo + 1) * S;
+    r.noisy0 = qn < L ? qn / BM : nQT;
+    r.nnoisy = nQT - r.noisy0;
+    // clean queries with block >= klo start at row klo*S
+    r.clean0 = (klo * S) / BM;
+    r.nclean = nQT - r.clean0;
+  }
+  return r;
+}
+
+}  // namespace bd

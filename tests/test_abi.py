@@ -1,0 +1,155 @@
+"""CPU checks of the C-ABI library: it loads, exports what include/bd_attn.h
+declares, its host tile classifier and tile walks agree with the oracle's
+explicit mask, and argument validation rejects bad calls before touching the
+device (these calls return before any HIP call, so no GPU is needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2512_22234_amd as bd
+from paper_2512_22234_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bd_attn.h")
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    names = sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(bd_attn_\w+)\s*\(", text, re.M)))
+    assert len(names) >= 7, names
+    L = _lib.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings():
+    assert bd.bd_attn_version() == 100
+    seen = set()
+    for st in range(5):
+        s = bd.bd_attn_status_string(st)
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 5
+    assert bd.bd_attn_status_string(99) == "unknown status"
+
+
+def _brute_classes(L, S, BM, BN):
+    M = oracle.visibility_mask(L, S)
+    nqt, nkt = -(-L // BM), -(-L // BN)
+    out = np.zeros((2 * nqt, 2 * nkt), dtype=np.int8)
+    for a in range(2 * nqt):
+        qh, i = divmod(a, nqt)
+        q0, q1 = qh * L + i * BM, qh * L + min(L, (i + 1) * BM)
+        for c in range(2 * nkt):
+            kh, j = divmod(c, nkt)
+            k0, k1 = kh * L + j * BN, kh * L + min(L, (j + 1) * BN)
+            blk = M[q0:q1, k0:k1]
+            full_size = (q1 - q0) == BM and (k1 - k0) == BN
+            if not blk.any():
+                out[a, c] = 0
+            elif blk.all() and full_size:
+                out[a, c] = 1
+            else:
+                out[a, c] = 2
+    return out
+
+
+CASES = [(L, S, BM, BN) for L in (1, 2, 5, 16, 33, 64, 100, 130, 257)
+         for S in (1, 2, 3, 4, 7, 16, 64, 1000)
+         for BM, BN in ((128, 64), (64, 128), (16, 16), (8, 32))]
+
+
+@pytest.mark.parametrize("L,S,BM,BN", CASES[::3] + [(2048, 4, 128, 64), (2048, 64, 64, 128), (300, 5, 128, 64)])
+def test_classifier_matches_explicit_mask(L, S, BM, BN):
+    got = bd.bd_attn_classify_tiles_host(L, S, BM, BN)
+    want = _brute_classes(L, S, BM, BN)
+    # soundness first (a wrong FULL/EMPTY would corrupt results), then exactness
+    assert not np.any((got == 1) & (want != 1)), "FULL claimed where a pair is hidden or tile ragged"
+    assert not np.any((got == 0) & (want != 0)), "EMPTY claimed where a pair is visible"
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("L,S,BM,BN", CASES[1::3] + [(2048, 4, 128, 64), (2048, 4, 64, 128), (8192, 4, 128, 64)])
+def test_tile_walks_visit_each_nonempty_pair_once(L, S, BM, BN):
+    cls = bd.bd_attn_classify_tiles_host(L, S, BM, BN)
+    for by_key in (False, True):
+        visits = bd.bd_attn_visit_lists_host(L, S, BM, BN, by_key)
+        np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"by_key={by_key}")
+
+
+def test_classifier_tile_counts_8b_shape():
+    # L=2048, S=4 with 128x128 tiles: per (b, h) 1024 pairs; 240 FULL, 48 PARTIAL, 736 EMPTY
+    c = bd.bd_attn_classify_tiles_host(2048, 4, 128, 128)
+    assert c.size == 1024
+    assert (c == 1).sum() == 240 and (c == 2).sum() == 48 and (c == 0).sum() == 736
+
+
+def test_workspace_bytes():
+    f = bd.bd_attn_workspace_bytes
+    assert f(2, 2048, 4, 32, 8, 128, 0, 0) > 0
+    assert f(2, 2048, 4, 32, 8, 128, 0, 1) > f(2, 2048, 4, 32, 8, 128, 0, 0)
+    assert f(1, 64, 4, 1, 1, 64, 1, 1) > f(1, 64, 4, 1, 1, 64, 0, 1)
+    assert f(2, 2048, 4, 32, 7, 128, 0, 0) == 0      # Hq % Hkv
+    assert f(2, 2048, 4, 32, 8, 96, 0, 0) == 0       # D unsupported
+    assert f(2, 0, 4, 32, 8, 128, 0, 0) == 0         # L < 1
+    assert f(2, 2048, 4, 32, 8, 128, 7, 0) == 0      # dtype
+
+
+# Fake, never-dereferenced device addresses: every call below fails validation
+# and returns before any HIP call.
+A = 1 << 40
+SZ = 1 << 32
+
+
+def _fwd(**kw):
+    a = dict(Q=A, K=A + SZ, V=A + 2 * SZ, B=1, L=64, S=4, Hq=2, Hkv=1, D=64, scale=0.0, dtype=0,
+             O=A + 3 * SZ, LSE=A + 4 * SZ, ws=A + 5 * SZ, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    L = _lib.lib()
+    vp = ctypes.c_void_p
+    return L.bd_attn_fwd(vp(a["Q"]), vp(a["K"]), vp(a["V"]), a["B"], a["L"], a["S"], a["Hq"], a["Hkv"],
+                         a["D"], a["scale"], a["dtype"], vp(a["O"]), vp(a["LSE"]), vp(a["ws"]),
+                         a["ws_bytes"], vp(a["stream"]))
+
+
+def _bwd(**kw):
+    a = dict(dO=A, Q=A + SZ, K=A + 2 * SZ, V=A + 3 * SZ, O=A + 4 * SZ, LSE=A + 5 * SZ, B=1, L=64, S=4,
+             Hq=2, Hkv=1, D=64, scale=0.0, dtype=0, dQ=A + 6 * SZ, dK=A + 7 * SZ, dV=A + 8 * SZ,
+             ws=A + 9 * SZ, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    L = _lib.lib()
+    vp = ctypes.c_void_p
+    return L.bd_attn_bwd(vp(a["dO"]), vp(a["Q"]), vp(a["K"]), vp(a["V"]), vp(a["O"]), vp(a["LSE"]),
+                         a["B"], a["L"], a["S"], a["Hq"], a["Hkv"], a["D"], a["scale"], a["dtype"],
+                         vp(a["dQ"]), vp(a["dK"]), vp(a["dV"]), vp(a["ws"]), a["ws_bytes"], vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=96), 2), (dict(D=256), 2), (dict(dtype=3), 2),
+    (dict(Hq=3, Hkv=2), 1), (dict(B=0), 1), (dict(L=0), 1), (dict(S=0), 1),
+    (dict(Q=0), 1), (dict(O=0), 1), (dict(LSE=0), 1), (dict(ws=0), 1),
+    (dict(Q=A + 8), 1), (dict(O=A + 3 * SZ + 2), 1), (dict(LSE=A + 4 * SZ + 2), 1),
+    (dict(O=A + 16), 1),                   # output overlaps Q
+    (dict(LSE=A + 3 * SZ + 64), 1),        # LSE overlaps O
+    (dict(ws=A + 2 * SZ + 32), 1),         # workspace overlaps V
+    (dict(ws_bytes=16), 3),
+    (dict(scale=float("nan")), 1),
+])
+def test_fwd_validation(kw, status):
+    assert _fwd(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=32), 2), (dict(Hq=4, Hkv=3), 1), (dict(dO=0), 1), (dict(dV=0), 1),
+    (dict(dQ=A + SZ + 16), 1),             # dQ overlaps Q
+    (dict(dK=A + 6 * SZ + 64), 1),         # dK overlaps dQ
+    (dict(dV=A + 5 * SZ), 1),              # dV overlaps LSE
+    (dict(dK=A + 7 * SZ + 4), 1),          # misaligned
+    (dict(ws_bytes=1000), 3),
+])
+def test_bwd_validation(kw, status):
+    assert _bwd(**kw) == status

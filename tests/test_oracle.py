@@ -315,3 +315,18 @@ def test_row_chunking_and_subsets_do_not_change_results():
         np.testing.assert_allclose(a, b, atol=1e-13, rtol=0)
     np.testing.assert_allclose(gs[0][1, 2:4], g[0][1, 2:4], atol=0, rtol=0)
     np.testing.assert_allclose(gs[1][1, 1], g[1][1, 1], atol=0, rtol=0)
+
+
+def test_sampled_matches_full_evaluation():
+    L, S, D, Hq, Hkv = 18, 4, 8, 4, 2
+    Q, K, V = _rand((2, Hq, 2 * L, D), 42), _rand((2, Hkv, 2 * L, D), 43), _rand((2, Hkv, 2 * L, D), 44)
+    dO = _rand((2, Hq, 2 * L, D), 45)
+    O, LSE = oracle.forward(Q, K, V, L, S)
+    dQ, dK, dV = oracle.backward(dO, Q, K, V, L, S)
+    qr, kr = [0, 5, 17, 18, 30, 35], [1, 4, 16, 20, 27, 35]
+    s = oracle.sampled(dO, Q, K, V, L, S, b=1, hkv=1, query_rows=qr, key_rows=kr, row_chunk=5)
+    np.testing.assert_allclose(s["O"], O[1, 2:4][:, qr], atol=1e-13, rtol=0)
+    np.testing.assert_allclose(s["LSE"], LSE[1, 2:4][:, qr], atol=1e-13, rtol=0)
+    np.testing.assert_allclose(s["dQ"], dQ[1, 2:4][:, qr], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(s["dK"], dK[1, 1, kr], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(s["dV"], dV[1, 1, kr], atol=1e-12, rtol=0)
