@@ -165,6 +165,7 @@ def main():
     tflops = (f_fwd + f_bwd) / (ms * 1e-3) / 1e12
     # algorithmic FLOPs of each kernel (useful work only; recomputation not counted)
     alg = {"fwd": 4 * w.D * npairs, "bwd_dkdv": 8 * w.D * npairs, "bwd_dq": 2 * w.D * npairs}
+    alg = {n: f for n, f in alg.items() if n in per}
     kernels = {}
     for name, t in per.items():
         entry = {"ms": round(t, 5)}

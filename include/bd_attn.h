@@ -55,7 +55,7 @@ enum bd_attn_status {
   BD_ATTN_OK = 0,
   BD_ATTN_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, B,L,S<1, Hq%Hkv!=0, overlap */
   BD_ATTN_ERR_UNSUPPORTED = 2,      /* D not in {64,128}, unknown dtype */
-  BD_ATTN_ERR_WORKSPACE_TOO_SMALL = 3,
+  BD_ATTN_ERR_WORKSPACE_TOO_SMALL = 3, /* checked before overlap with the workspace */
   BD_ATTN_ERR_HIP = 4               /* a HIP launch reported an error */
 };
 
@@ -68,7 +68,8 @@ enum bd_attn_tile_class { BD_TILE_EMPTY = 0, BD_TILE_FULL = 1, BD_TILE_PARTIAL =
  * Forward pass (Section 4.1; masking rules of Eq. 1 and Eq. 2).
  * Inputs Q, K, V; outputs O (same dtype as the inputs) and LSE (float32).
  * ws/ws_bytes: device workspace of at least
- * bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, dtype, 0) bytes.
+ * bd_attn_workspace_bytes(B, L, S, Hq, Hkv, D, dtype, 0) bytes (zero for
+ * bfloat16 inputs; ws may then be NULL).
  */
 int bd_attn_fwd(const void* Q, const void* K, const void* V,
                 int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,

@@ -17,7 +17,7 @@ constexpr int kVersion = 100;  // 0.1.0
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t kvt = 0, delta = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
+  size_t delta = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
 };
 
 bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
@@ -27,14 +27,13 @@ bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
 Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
   Layout w;
   const size_t N = 2 * (size_t)L;
-  const size_t Lp = (size_t)bd::cdiv(L, bd::KEY_PAD) * bd::KEY_PAD;
   const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
   size_t off = 0;
-  w.kvt = off;
-  off += align256((size_t)B * Hkv * D * 2 * Lp * 2);
   if (bwd) {
     w.delta = off;
     off += align256((size_t)B * Hq * N * 4);
+    w.part = off;
+    off += align256(bd::dkdv_partial_floats(B, Hkv, L, D) * 4);
   }
   if (dtype == BD_ATTN_FP32) {
     w.q = off; off += align256(nq * 2);
@@ -77,7 +76,6 @@ int validate(int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype
   s.Hkv = Hkv;
   s.D = D;
   s.G = Hq / Hkv;
-  s.Lp = bd::cdiv(L, bd::KEY_PAD) * bd::KEY_PAD;
   s.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)D);
   return BD_ATTN_OK;
 }
@@ -211,9 +209,9 @@ int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void*
 
 const char* bd_attn_stage_names(int for_bwd, int dtype) {
   if (dtype == BD_ATTN_FP32)
-    return for_bwd ? "cast_q,cast_k,cast_v,cast_o,cast_do,bwd_pre,transpose_k,bwd_dkdv,bwd_dq,cast_dq,cast_dk,cast_dv"
-                   : "cast_q,cast_k,cast_v,transpose_v,fwd,cast_o";
-  return for_bwd ? "bwd_pre,transpose_k,bwd_dkdv,bwd_dq" : "transpose_v,fwd";
+    return for_bwd ? "cast_q,cast_k,cast_v,cast_o,cast_do,bwd_pre,bwd_dkdv,bwd_dkdv_combine,bwd_dq,cast_dq,cast_dk,cast_dv"
+                   : "cast_q,cast_k,cast_v,fwd,cast_o";
+  return for_bwd ? "bwd_pre,bwd_dkdv,bwd_dkdv_combine,bwd_dq" : "fwd";
 }
 
 }  // extern "C"
@@ -226,14 +224,15 @@ int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, i
   bd::Shape s;
   const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
   if (st != BD_ATTN_OK) return st;
-  if (!Q || !K || !V || !O || !LSE || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, false);
+  if (!Q || !K || !V || !O || !LSE || (w.total > 0 && !ws)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4) ||
       !aligned(ws, 16))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
   const size_t N = 2 * (size_t)L;
   const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
-  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, false);
   const Range in[] = {{Q, nq * esz}, {K, nk * esz}, {V, nk * esz}};
   const Range out[] = {{O, nq * esz}, {LSE, (size_t)B * Hq * N * 4}, {ws, w.total}};
   for (const Range& o : out)
@@ -241,7 +240,6 @@ int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, i
       if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2]))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
-  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
 
   (void)hipGetLastError();  // clear a stale error so it is not reported as ours
   BD_TRY(marks.rec(stream));
@@ -257,8 +255,7 @@ int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, i
     v = wb + w.v;
     o = wb + w.o;
   }
-  BD_LAUNCH(bd::launch_transpose_keys(v, wb + w.kvt, B * Hkv, L, s.Lp, D, stream));
-  BD_LAUNCH(bd::launch_fwd(s, q, k, wb + w.kvt, o, LSE, stream));
+  BD_LAUNCH(bd::launch_fwd(s, q, k, v, o, LSE, stream));
   if (dtype == BD_ATTN_FP32) BD_LAUNCH(bd::launch_cast_bf16_to_f32(o, static_cast<float*>(O), nq, stream));
   return BD_ATTN_OK;
 }
@@ -269,14 +266,16 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
   bd::Shape s;
   const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
   if (st != BD_ATTN_OK) return st;
-  if (!dO || !Q || !K || !V || !O || !LSE || !dQ || !dK || !dV || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, true);
+  if (!dO || !Q || !K || !V || !O || !LSE || !dQ || !dK || !dV || (w.total > 0 && !ws))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(dO, 16) || !aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
       !aligned(LSE, 4) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) || !aligned(ws, 16))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
   const size_t N = 2 * (size_t)L;
   const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
-  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, true);
   const Range in[] = {{dO, nq * esz}, {Q, nq * esz}, {K, nk * esz}, {V, nk * esz}, {O, nq * esz},
                       {LSE, (size_t)B * Hq * N * 4}};
   const Range out[] = {{dQ, nq * esz}, {dK, nk * esz}, {dV, nk * esz}, {ws, w.total}};
@@ -286,7 +285,6 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
   for (int a = 0; a < 4; ++a)
     for (int c = a + 1; c < 4; ++c)
       if (overlap(out[a], out[c])) return BD_ATTN_ERR_INVALID_ARGUMENT;
-  if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
 
   (void)hipGetLastError();
   BD_TRY(marks.rec(stream));
@@ -310,9 +308,10 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
   }
   float* delta = reinterpret_cast<float*>(wb + w.delta);
   BD_LAUNCH(bd::launch_bwd_pre(s, o, g, delta, stream));
-  BD_LAUNCH(bd::launch_transpose_keys(k, wb + w.kvt, B * Hkv, L, s.Lp, D, stream));
-  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, LSE, delta, dk, dv, stream));
-  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, wb + w.kvt, v, g, LSE, delta, dq, stream));
+  float* part = reinterpret_cast<float*>(wb + w.part);
+  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, LSE, delta, dk, dv, part, stream));
+  BD_LAUNCH(bd::launch_bwd_dkdv_combine(s, part, dk, dv, stream));
+  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, LSE, delta, dq, stream));
   if (dtype == BD_ATTN_FP32) {
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));

@@ -8,17 +8,21 @@
 //   dK    = scale dS^T Q                                (dkdv, key-tile major)
 //   dQ    = scale dS K                                  (dq, query-tile major)
 //
-// dkdv: one workgroup owns a (batch, KV head, 128-key tile); each of its four
+// dkdv: a workgroup owns a (batch, KV head, 128-key tile); each of its four
 // waves owns 32 keys whose K/V rows stay in registers.  It walks the query
-// heads of the GQA group and the query tiles (64 rows) that can see the key
-// tile, in the order given by the exact tile classification.  Scores are
-// computed as S = Q K^T so each lane owns one key column; P and dS are then
-// the B operands of dV^T = dO^T P and dK^T = Q^T dS directly, with Q^T and
-// dO^T written to LDS (perm16 order) next to the row-major tiles.
+// heads of the GQA group and the 64-row query tiles that can see the key tile
+// (the exact tile classification gives the list).  Scores are S = Q K^T so
+// each lane owns one key column; P and dS are then directly the B operands of
+// dV^T = dO^T P and dK^T = Q^T dS, whose A operands come from the row-major Q
+// and dO tiles through the transposing LDS read.  Work per clean key tile
+// shrinks linearly with its position, so each clean tile's walk is split into
+// two halves run by two workgroups that write float32 partial sums; a combine
+// kernel adds the two halves in a fixed order.  Noisy key tiles (seen only by
+// their own block's noisy queries) are done by one workgroup each.
 //
-// dq: one workgroup owns a (batch, query head, 128-row query tile) like the
-// forward; scores are S^T = K Q^T (lane = query), dQ^T = K^T dS^T with K^T
-// from the transposed copy.
+// dq: a workgroup owns a (batch, query head, 128-row query tile) like the
+// forward; scores are S^T = K Q^T (lane = query) and dQ^T = K^T dS^T with K^T
+// read from the row-major K tile through the transposing LDS read.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -57,6 +61,7 @@ struct DkvParams {
   const float* delta;
   bf16* dK;
   bf16* dV;
+  float* part;  // [2 halves][2 (dK, dV)][B*Hkv][L][D] partial sums of clean key tiles
   int L, S, Hq, Hkv, G, nKT, nkv;
   float c;      // scale * log2(e)
   float scale;
@@ -65,22 +70,19 @@ struct DkvParams {
 template <int D>
 struct DkvSmem {
   static constexpr int BM = DKV_BM;
-  static constexpr int QS = D + 8;   // row-major tile stride (elements)
-  static constexpr int TS = BM + 8;  // transposed tile stride
+  static constexpr int QS = D + 8;  // row stride (elements)
   bf16 q[2][BM * QS];
   bf16 dO[2][BM * QS];
-  uint16_t qt[2][D * TS];
-  uint16_t dot[2][D * TS];
-  float lse2[2][BM];
-  float dlt[2][BM];
-  int qblk[2][BM];
+  alignas(16) float lse2[2][BM];
+  alignas(16) float dlt[2][BM];
+  alignas(16) int qblk[2][BM];
 };
 
 template <int D>
 __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   constexpr int BM = DKV_BM, BN = DKV_BN;
   constexpr int DS = D / 16, DB = D / 32, QB = BM / 32, PC = BM / 16;
-  constexpr int QS = DkvSmem<D>::QS, TS = DkvSmem<D>::TS;
+  constexpr int QS = DkvSmem<D>::QS;
   constexpr int NCH = BM * D / 8 / 256;  // 16-byte chunks per thread, for each of Q and dO
   static_assert(NCH * 256 * 8 == BM * D, "tile must split evenly over 256 threads");
   __shared__ DkvSmem<D> sm;
@@ -89,13 +91,16 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int l32 = lane & 31, g2 = lane >> 5;
   const int L = p.L, S = p.S, N = 2 * L;
 
-  // Clean key tiles first, lowest index (most query tiles) first; the light
-  // noisy key tiles last.  Consecutive workgroups are different KV heads.
+  // Items: clean key tiles in ascending index (most work first), each as two
+  // halves of its walk; then noisy key tiles, one item each.  Consecutive
+  // workgroups are different KV heads.
   const int id = blockIdx.x;
   const int rank = id / p.nkv;
   const int grp = id - rank * p.nkv;  // b * Hkv + hk
-  const int kh = rank < p.nKT ? HALF_CLEAN : HALF_NOISY;
-  const int j = rank < p.nKT ? rank : rank - p.nKT;
+  const bool clean = rank < 2 * p.nKT;
+  const int kh = clean ? HALF_CLEAN : HALF_NOISY;
+  const int j = clean ? (rank >> 1) : rank - 2 * p.nKT;
+  const int split = clean ? (rank & 1) : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
   const int k0 = j * BN, k1 = imin(L, k0 + BN);
 
@@ -113,7 +118,9 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
 
   const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
   const int per_g = ql.count();
-  const int T = p.G * per_g;
+  const int Tall = p.G * per_g;
+  const int t0 = clean ? (split * Tall) / 2 : 0;
+  const int t1 = clean ? ((split + 1) * Tall) / 2 : Tall;
 
   u32x4 qst[NCH], dost[NCH];
   float lse_st = 0.f, dlt_st = 0.f;
@@ -123,21 +130,20 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
     int qh, i;
     ql.at(t - g * per_g, qh, i);
     const size_t bhq = (size_t)b * p.Hq + hk * p.G + g;
+    const size_t hbase = (bhq * N + qh * L) * D;
 #pragma unroll
     for (int u = 0; u < NCH; ++u) {
       const int c = tid + 256 * u;
       const int row = c / (D / 8), col8 = c % (D / 8);
-      const int qr = i * BM + row;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      const size_t off = (bhq * N + qh * L + qr) * D + col8 * 8;
-      qst[u] = qr < L ? ld16(p.Q + off) : z;
-      dost[u] = qr < L ? ld16(p.dO + off) : z;
+      qst[u] = ld16_rows(p.Q + hbase, i * BM + row, L, D, col8 * 8);
+      dost[u] = ld16_rows(p.dO + hbase, i * BM + row, L, D, col8 * 8);
     }
     if (tid < BM) {
       const int qr = i * BM + tid;
       const bool ok = qr < L;
-      lse_st = ok ? p.LSE[bhq * N + qh * L + qr] * LOG2E : 0.f;
-      dlt_st = ok ? p.delta[bhq * N + qh * L + qr] : 0.f;
+      const size_t rr = bhq * N + qh * L + (ok ? qr : L - 1);
+      lse_st = p.LSE[rr];  // rows past the end are masked (qblk invalid)
+      dlt_st = p.delta[rr];
       qb_st = ok ? qr / S : QBLK_INVALID;
     }
   };
@@ -148,16 +154,9 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
       const int row = c / (D / 8), col8 = c % (D / 8);
       st16(&sm.q[buf][row * QS + col8 * 8], qst[u]);
       st16(&sm.dO[buf][row * QS + col8 * 8], dost[u]);
-      const int pr = perm16(row);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = col8 * 8 + e;
-        sm.qt[buf][d * TS + pr] = (uint16_t)(qst[u][e >> 1] >> (16 * (e & 1)));
-        sm.dot[buf][d * TS + pr] = (uint16_t)(dost[u][e >> 1] >> (16 * (e & 1)));
-      }
     }
     if (tid < BM) {
-      sm.lse2[buf][tid] = lse_st;
+      sm.lse2[buf][tid] = lse_st * LOG2E;
       sm.dlt[buf][tid] = dlt_st;
       sm.qblk[buf][tid] = qb_st;
     }
@@ -172,15 +171,16 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
       dvacc[db][e] = 0.f;
     }
 
-  if (T > 0) {
-    load_tile(0);
+  if (t0 < t1) {
+    load_tile(t0);
     store_tile(0);
   }
+  wait_global_loads();  // K/V rows are in registers; the loop only waits on its own prefetch
   __syncthreads();
 
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < T) load_tile(t + 1);
+  for (int t = t0; t < t1; ++t) {
+    const int buf = (t - t0) & 1;
+    if (t + 1 < t1) load_tile(t + 1);
     const int g = t / per_g;
     int qh, i;
     ql.at(t - g * per_g, qh, i);
@@ -206,6 +206,7 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
           dpacc[qb] = mfma32(ad, vreg[s], dpacc[qb]);
         }
       const bool partial = cls == TILE_PARTIAL;
+      const BlockWindow win = query_window(qh, kh, bk);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -213,10 +214,12 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
           const int rr = qb * 32 + 8 * i4 + 4 * g2;
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sm.lse2[buf][rr]);
           const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sm.dlt[buf][rr]);
+          const int4 qb4 = *reinterpret_cast<const int4*>(&sm.qblk[buf][rr]);
+          const int qbv[4] = {qb4.x, qb4.y, qb4.z, qb4.w};
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             float pv = fast_exp2(sacc[qb][4 * i4 + jj] * p.c - l4[jj]);
-            if (partial && !visible(qh, sm.qblk[buf][rr + jj], kh, bk)) pv = 0.f;
+            pv = (!partial || win.has(qbv[jj])) ? pv : 0.f;
             dpacc[qb][4 * i4 + jj] = pv * (dpacc[qb][4 * i4 + jj] - d4[jj]);
             sacc[qb][4 * i4 + jj] = pv;
           }
@@ -232,20 +235,37 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 ad = *reinterpret_cast<const bf16x8*>(&sm.dot[buf][(db * 32 + l32) * TS + 16 * c + 8 * g2]);
+          const bf16x8 ad = lds_read_tr(sm.dO[buf], QS, 16 * c, db * 32, lane);
           dvacc[db] = mfma32(ad, pb[c], dvacc[db]);
-          const bf16x8 aq = *reinterpret_cast<const bf16x8*>(&sm.qt[buf][(db * 32 + l32) * TS + 16 * c + 8 * g2]);
+          const bf16x8 aq = lds_read_tr(sm.q[buf], QS, 16 * c, db * 32, lane);
           dkacc[db] = mfma32(aq, dsb[c], dkacc[db]);
         }
     }
-    if (t + 1 < T) store_tile(buf ^ 1);
+    compute_fence();
+    if (t + 1 < t1) store_tile(buf ^ 1);
     __syncthreads();
   }
 
-  if (kvalid) {
+  if (!kvalid) return;
+  const float sc = p.scale;
+  if (clean) {
+    // float32 partial sums; the combine kernel adds the two halves
+    const size_t plane = (size_t)p.nkv * L * D;
+    float* pk = p.part + (size_t)(2 * split) * plane + ((size_t)grp * L + kk) * D + 4 * g2;
+    float* pv = pk + plane;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 vk = {dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc, dkacc[db][4 * i + 2] * sc,
+                          dkacc[db][4 * i + 3] * sc};
+        const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
+        *reinterpret_cast<f32x4*>(pk + db * 32 + 8 * i) = vk;
+        *reinterpret_cast<f32x4*>(pv + db * 32 + 8 * i) = vv;
+      }
+  } else {
     bf16* dkp = p.dK + krow * D + 4 * g2;
     bf16* dvp = p.dV + krow * D + 4 * g2;
-    const float sc = p.scale;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -258,17 +278,37 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   }
 }
 
+// dK/dV of the clean half = half0 + half1 (fixed order), rounded to bf16.
+// One thread per 4 consecutive features.
+__global__ __launch_bounds__(256) void dkdv_combine_kernel(const float* __restrict__ part, bf16* __restrict__ dK,
+                                                           bf16* __restrict__ dV, int nkv, int L, int D) {
+  const size_t plane = (size_t)nkv * L * D;
+  const size_t quads = plane / 4;
+  const size_t stride = (size_t)gridDim.x * 256;
+  for (size_t qd = (size_t)blockIdx.x * 256 + threadIdx.x; qd < quads; qd += stride) {
+    const size_t e = qd * 4;
+    const size_t row = e / D;  // grp * L + key
+    const size_t grp = row / L, key = row - grp * L;
+    const size_t out = ((grp * 2 + 1) * L + key) * D + (e - row * D);
+    const f32x4 k0 = *reinterpret_cast<const f32x4*>(part + e);
+    const f32x4 v0 = *reinterpret_cast<const f32x4*>(part + plane + e);
+    const f32x4 k1 = *reinterpret_cast<const f32x4*>(part + 2 * plane + e);
+    const f32x4 v1 = *reinterpret_cast<const f32x4*>(part + 3 * plane + e);
+    st_bf16x4(dK + out, k0[0] + k1[0], k0[1] + k1[1], k0[2] + k1[2], k0[3] + k1[3]);
+    st_bf16x4(dV + out, v0[0] + v1[0], v0[1] + v1[1], v0[2] + v1[2], v0[3] + v1[3]);
+  }
+}
+
 // ----------------------------------------------------------------------------
 struct DqParams {
   const bf16* Q;
   const bf16* K;
-  const bf16* Kt;
   const bf16* V;
   const bf16* dO;
   const float* LSE;
   const float* delta;
   bf16* dQ;
-  int L, S, Hq, Hkv, G, Lp, nQT, nbh;
+  int L, S, Hq, Hkv, G, nQT, nbh;
   float c;
   float scale;
 };
@@ -277,18 +317,16 @@ template <int D>
 struct DqSmem {
   static constexpr int BN = DQ_BN;
   static constexpr int KS = D + 8;
-  static constexpr int VS = BN + 8;
   bf16 k[2][BN * KS];
   bf16 v[2][BN * KS];
-  bf16 kt[2][D * VS];
-  int kblk[2][BN];
+  alignas(16) int kblk[2][BN];
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
+__global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   constexpr int BM = DQ_BM, BN = DQ_BN;
   constexpr int DS = D / 16, DB = D / 32, KB = BN / 32, PC = BN / 16;
-  constexpr int KS = DqSmem<D>::KS, VS = DqSmem<D>::VS;
+  constexpr int KS = DqSmem<D>::KS;
   constexpr int NCH = BN * D / 8 / 256;
   static_assert(NCH * 256 * 8 == BN * D, "tile must split evenly over 256 threads");
   __shared__ DqSmem<D> sm;
@@ -306,7 +344,6 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
 
   const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
-  const bf16* Ktp = p.Kt + (size_t)(b * p.Hkv + hk) * D * (2 * p.Lp);
 
   const int r = q0 + w * 32 + l32;
   const bool qvalid = r < q1;
@@ -326,22 +363,19 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
 
-  u32x4 kst[NCH], vst[NCH], tst[NCH];
+  u32x4 kst[NCH], vst[NCH];
   int kbst = 0;
   auto load_tile = [&](int t) {
     int kh, j;
     kl.at(t, kh, j);
+    const bf16* kp = p.K + kvbase + (size_t)kh * L * D;
+    const bf16* vp = p.V + kvbase + (size_t)kh * L * D;
 #pragma unroll
     for (int u = 0; u < NCH; ++u) {
       const int c = tid + 256 * u;
       const int row = c / (D / 8), col8 = c % (D / 8);
-      const int key = j * BN + row;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      const size_t off = kvbase + (size_t)(kh * L + key) * D + col8 * 8;
-      kst[u] = key < L ? ld16(p.K + off) : z;
-      vst[u] = key < L ? ld16(p.V + off) : z;
-      const int d = c / (BN / 8), kc = c % (BN / 8);
-      tst[u] = ld16(Ktp + (size_t)d * (2 * p.Lp) + kh * p.Lp + j * BN + kc * 8);
+      kst[u] = ld16_rows(kp, j * BN + row, L, D, col8 * 8);
+      vst[u] = ld16_rows(vp, j * BN + row, L, D, col8 * 8);
     }
     if (tid < BN) {
       const int key = j * BN + tid;
@@ -355,8 +389,6 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
       const int row = c / (D / 8), col8 = c % (D / 8);
       st16(&sm.k[buf][row * KS + col8 * 8], kst[u]);
       st16(&sm.v[buf][row * KS + col8 * 8], vst[u]);
-      const int d = c / (BN / 8), kc = c % (BN / 8);
-      st16(&sm.kt[buf][d * VS + kc * 8], tst[u]);
     }
     if (tid < BN) sm.kblk[buf][tid] = kbst;
   };
@@ -371,6 +403,7 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
     load_tile(0);
     store_tile(0);
   }
+  wait_global_loads();  // Q/dO rows are in registers; the loop only waits on its own prefetch
   __syncthreads();
 
   for (int t = 0; t < T; ++t) {
@@ -400,16 +433,18 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
           dpacc[kb] = mfma32(av, doreg[s], dpacc[kb]);
         }
       const bool partial = cls == TILE_PARTIAL;
+      const BlockWindow win = key_window(qh, kh, bq);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int* kbp = &sm.kblk[buf][kb * 32 + 8 * i + 4 * g2];
+          const int4 kb4 = *reinterpret_cast<const int4*>(&sm.kblk[buf][kb * 32 + 8 * i + 4 * g2]);
+          const int kbv[4] = {kb4.x, kb4.y, kb4.z, kb4.w};
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             const int e = 4 * i + jj;
             float pv = fast_exp2(sacc[kb][e] * p.c - lse2);
-            if (partial && !visible(qh, bq, kh, kbp[jj])) pv = 0.f;
+            pv = (!partial || win.has(kbv[jj])) ? pv : 0.f;
             sacc[kb][e] = pv * (dpacc[kb][e] - dlt);
           }
         }
@@ -421,10 +456,11 @@ __global__ __launch_bounds__(256, 1) void dq_kernel(DqParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 a = lds_bf16x8(&sm.kt[buf][(db * 32 + l32) * VS + 16 * c + 8 * g2]);
+          const bf16x8 a = lds_read_tr(sm.k[buf], KS, 16 * c, db * 32, lane);
           dqacc[db] = mfma32(a, dsb[c], dqacc[db]);
         }
     }
+    compute_fence();
     if (t + 1 < T) store_tile(buf ^ 1);
     __syncthreads();
   }
@@ -453,7 +489,7 @@ hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, float* de
 
 template <int D>
 hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* LSE, const float* delta, void* dK, void* dV, hipStream_t st) {
+                         const float* LSE, const float* delta, void* dK, void* dV, float* part, hipStream_t st) {
   DkvParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
@@ -463,6 +499,7 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.delta = delta;
   p.dK = static_cast<bf16*>(dK);
   p.dV = static_cast<bf16*>(dV);
+  p.part = part;
   p.L = s.L;
   p.S = s.S;
   p.Hq = s.Hq;
@@ -472,18 +509,17 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.nkv = s.B * s.Hkv;
   p.c = s.scale * LOG2E;
   p.scale = s.scale;
-  const dim3 grid(2 * p.nKT * p.nkv);
+  const dim3 grid(3 * p.nKT * p.nkv);
   hipLaunchKernelGGL(dkdv_kernel<D>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
 template <int D>
-hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* Kt, const void* V,
-                       const void* dO, const float* LSE, const float* delta, void* dQ, hipStream_t st) {
+hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
+                       const float* LSE, const float* delta, void* dQ, hipStream_t st) {
   DqParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
-  p.Kt = static_cast<const bf16*>(Kt);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
   p.LSE = LSE;
@@ -494,7 +530,6 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
   p.Hq = s.Hq;
   p.Hkv = s.Hkv;
   p.G = s.G;
-  p.Lp = s.Lp;
   p.nQT = cdiv(s.L, DQ_BM);
   p.nbh = s.B * s.Hq;
   p.c = s.scale * LOG2E;
@@ -512,15 +547,26 @@ hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, float* 
 }
 
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                           const float* LSE, const float* delta, void* dK, void* dV, hipStream_t st) {
-  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, LSE, delta, dK, dV, st);
-  return launch_dkdv_d<64>(s, Q, K, V, dO, LSE, delta, dK, dV, st);
+                           const float* LSE, const float* delta, void* dK, void* dV, float* part,
+                           hipStream_t st) {
+  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, LSE, delta, dK, dV, part, st);
+  return launch_dkdv_d<64>(s, Q, K, V, dO, LSE, delta, dK, dV, part, st);
 }
 
-hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* Kt, const void* V,
-                         const void* dO, const float* LSE, const float* delta, void* dQ, hipStream_t st) {
-  if (s.D == 128) return launch_dq_d<128>(s, Q, K, Kt, V, dO, LSE, delta, dQ, st);
-  return launch_dq_d<64>(s, Q, K, Kt, V, dO, LSE, delta, dQ, st);
+hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, void* dV, hipStream_t st) {
+  const int nkv = s.B * s.Hkv;
+  const size_t quads = (size_t)nkv * s.L * s.D / 4;
+  size_t blocks = (quads + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(dkdv_combine_kernel, dim3((unsigned)blocks), dim3(256), 0, st, part, static_cast<bf16*>(dK),
+                     static_cast<bf16*>(dV), nkv, s.L, s.D);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
+                         const float* LSE, const float* delta, void* dQ, hipStream_t st) {
+  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, LSE, delta, dQ, st);
+  return launch_dq_d<64>(s, Q, K, V, dO, LSE, delta, dQ, st);
 }
 
 }  // namespace bd

@@ -6,13 +6,13 @@
 // that each lane owns one query column: the row max needs one cross-lane
 // exchange (lane l <-> l+32) per key tile and the running row sum stays a
 // per-lane partial until the epilogue.  O^T = V^T P^T reuses the score
-// accumulator directly as the bf16 B operand; V^T comes from a transposed
-// copy whose keys are stored in perm16 order (see device.hpp).
+// accumulator directly as the bf16 B operand; its A operand V^T is read from
+// the row-major V tile with the transposing LDS read (see device.hpp).
 //
 // Key tiles (64 keys) are visited in the order given by the exact tile
 // classification: FULL tiles run with no per-element test, PARTIAL tiles
 // apply the visibility rule per element, EMPTY tiles are never loaded.  K and
-// V^T tiles are double-buffered in LDS; the next tile's global loads are in
+// V tiles are double-buffered in LDS; the next tile's global loads are in
 // flight while the current one is computed.
 #include "device.hpp"
 #include "kernels.hpp"
@@ -23,29 +23,28 @@ namespace {
 struct FwdParams {
   const bf16* Q;
   const bf16* K;
-  const bf16* Vt;
+  const bf16* V;
   bf16* O;
   float* LSE;
-  int L, S, Hq, Hkv, G, Lp, nQT, nbh;
+  int L, S, Hq, Hkv, G, nQT, nbh;
   float c;  // scale * log2(e)
 };
 
 template <int D>
 struct FwdSmem {
   static constexpr int BN = FWD_BN;
-  static constexpr int KS = D + 8;   // K row stride (elements), 16-byte pad against bank conflicts
-  static constexpr int VS = BN + 8;  // V^T row stride
+  static constexpr int KS = D + 8;  // K/V row stride (elements), 16-byte pad against bank conflicts
   bf16 k[2][BN * KS];
-  bf16 vt[2][D * VS];
-  int kblk[2][BN];
+  bf16 v[2][BN * KS];
+  alignas(16) int kblk[2][BN];
 };
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   constexpr int BM = FWD_BM, BN = FWD_BN;
   constexpr int DS = D / 16, DB = D / 32, KB = BN / 32, PC = BN / 16;
-  constexpr int KS = FwdSmem<D>::KS, VS = FwdSmem<D>::VS;
-  constexpr int NCH = BN * D / 8 / 256;  // 16-byte chunks per thread, for each of K and V^T
+  constexpr int KS = FwdSmem<D>::KS;
+  constexpr int NCH = BN * D / 8 / 256;  // 16-byte chunks per thread, for each of K and V
   static_assert(NCH * 256 * 8 == BN * D, "tile must split evenly over 256 threads");
   __shared__ FwdSmem<D> sm;
 
@@ -63,8 +62,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
 
-  const bf16* Kp = p.K + (size_t)(b * p.Hkv + hk) * N * D;
-  const bf16* Vtp = p.Vt + (size_t)(b * p.Hkv + hk) * D * (2 * p.Lp);
+  const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
 
   const int r = q0 + w * 32 + l32;  // this lane's query row (local to its half)
   const bool qvalid = r < q1;
@@ -87,15 +85,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   auto load_tile = [&](int t) {
     int kh, j;
     kl.at(t, kh, j);
+    const bf16* kp = p.K + kvbase + (size_t)kh * L * D;
+    const bf16* vp = p.V + kvbase + (size_t)kh * L * D;
 #pragma unroll
     for (int u = 0; u < NCH; ++u) {
       const int c = tid + 256 * u;
       const int row = c / (D / 8), col8 = c % (D / 8);
-      const int key = j * BN + row;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      kst[u] = key < L ? ld16(Kp + (size_t)(kh * L + key) * D + col8 * 8) : z;
-      const int d = c / (BN / 8), kc = c % (BN / 8);
-      vst[u] = ld16(Vtp + (size_t)d * (2 * p.Lp) + kh * p.Lp + j * BN + kc * 8);
+      kst[u] = ld16_rows(kp, j * BN + row, L, D, col8 * 8);
+      vst[u] = ld16_rows(vp, j * BN + row, L, D, col8 * 8);
     }
     if (tid < BN) {
       const int key = j * BN + tid;
@@ -108,8 +105,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       const int c = tid + 256 * u;
       const int row = c / (D / 8), col8 = c % (D / 8);
       st16(&sm.k[buf][row * KS + col8 * 8], kst[u]);
-      const int d = c / (BN / 8), kc = c % (BN / 8);
-      st16(&sm.vt[buf][d * VS + kc * 8], vst[u]);
+      st16(&sm.v[buf][row * KS + col8 * 8], vst[u]);
     }
     if (tid < BN) sm.kblk[buf][tid] = kbst;
   };
@@ -125,6 +121,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
     load_tile(0);
     store_tile(0);
   }
+  wait_global_loads();  // Q rows are in registers; the loop only waits on its own prefetch
   __syncthreads();
 
   for (int t = 0; t < T; ++t) {
@@ -149,14 +146,16 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
           sacc[kb] = mfma32(a, qreg[s], sacc[kb]);
         }
       if (cls == TILE_PARTIAL) {
+        const BlockWindow win = key_window(qh, kh, bq);
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int* kbp = &sm.kblk[buf][kb * 32 + 8 * i + 4 * g2];
+            const int4 kb4 = *reinterpret_cast<const int4*>(&sm.kblk[buf][kb * 32 + 8 * i + 4 * g2]);
+            const int kbv[4] = {kb4.x, kb4.y, kb4.z, kb4.w};
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj)
-              if (!visible(qh, bq, kh, kbp[jj])) sacc[kb][4 * i + jj] = -INFINITY;
+              sacc[kb][4 * i + jj] = win.has(kbv[jj]) ? sacc[kb][4 * i + jj] : -INFINITY;
           }
       }
       float mx = -INFINITY;
@@ -191,10 +190,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 a = lds_bf16x8(&sm.vt[buf][(db * 32 + l32) * VS + 16 * c + 8 * g2]);
+          const bf16x8 a = lds_read_tr(sm.v[buf], KS, 16 * c, db * 32, lane);
           oacc[db] = mfma32(a, pb[c], oacc[db]);
         }
     }
+    compute_fence();
     if (t + 1 < T) store_tile(buf ^ 1);
     __syncthreads();
   }
@@ -214,12 +214,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 }
 
 template <int D>
-hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void* Vt, void* O,
+hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void* V, void* O,
                         float* LSE, hipStream_t st) {
   FwdParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
-  p.Vt = static_cast<const bf16*>(Vt);
+  p.V = static_cast<const bf16*>(V);
   p.O = static_cast<bf16*>(O);
   p.LSE = LSE;
   p.L = s.L;
@@ -227,7 +227,6 @@ hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void
   p.Hq = s.Hq;
   p.Hkv = s.Hkv;
   p.G = s.G;
-  p.Lp = s.Lp;
   p.nQT = cdiv(s.L, FWD_BM);
   p.nbh = s.B * s.Hq;
   p.c = s.scale * LOG2E;
@@ -238,10 +237,10 @@ hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void
 
 }  // namespace
 
-hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* Vt, void* O,
+hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* V, void* O,
                       float* LSE, hipStream_t st) {
-  if (s.D == 128) return launch_fwd_d<128>(s, Q, K, Vt, O, LSE, st);
-  return launch_fwd_d<64>(s, Q, K, Vt, O, LSE, st);
+  if (s.D == 128) return launch_fwd_d<128>(s, Q, K, V, O, LSE, st);
+  return launch_fwd_d<64>(s, Q, K, V, O, LSE, st);
 }
 
 }  // namespace bd

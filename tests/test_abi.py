@@ -90,8 +90,9 @@ def test_classifier_tile_counts_8b_shape():
 
 def test_workspace_bytes():
     f = bd.bd_attn_workspace_bytes
-    assert f(2, 2048, 4, 32, 8, 128, 0, 0) > 0
-    assert f(2, 2048, 4, 32, 8, 128, 0, 1) > f(2, 2048, 4, 32, 8, 128, 0, 0)
+    assert f(2, 2048, 4, 32, 8, 128, 0, 0) == 0      # bf16 forward needs no workspace
+    assert f(2, 2048, 4, 32, 8, 128, 0, 1) > 0
+    assert f(1, 64, 4, 1, 1, 64, 1, 0) > 0
     assert f(1, 64, 4, 1, 1, 64, 1, 1) > f(1, 64, 4, 1, 1, 64, 0, 1)
     assert f(2, 2048, 4, 32, 7, 128, 0, 0) == 0      # Hq % Hkv
     assert f(2, 2048, 4, 32, 8, 96, 0, 0) == 0       # D unsupported
@@ -100,13 +101,14 @@ def test_workspace_bytes():
 
 
 # Fake, never-dereferenced device addresses: every call below fails validation
-# and returns before any HIP call.
+# and returns before any HIP call (the defaults use the float32 path so that
+# the workspace is non-empty and the workspace checks are exercised).
 A = 1 << 40
 SZ = 1 << 32
 
 
 def _fwd(**kw):
-    a = dict(Q=A, K=A + SZ, V=A + 2 * SZ, B=1, L=64, S=4, Hq=2, Hkv=1, D=64, scale=0.0, dtype=0,
+    a = dict(Q=A, K=A + SZ, V=A + 2 * SZ, B=1, L=64, S=4, Hq=2, Hkv=1, D=64, scale=0.0, dtype=1,
              O=A + 3 * SZ, LSE=A + 4 * SZ, ws=A + 5 * SZ, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     L = _lib.lib()
@@ -118,7 +120,7 @@ def _fwd(**kw):
 
 def _bwd(**kw):
     a = dict(dO=A, Q=A + SZ, K=A + 2 * SZ, V=A + 3 * SZ, O=A + 4 * SZ, LSE=A + 5 * SZ, B=1, L=64, S=4,
-             Hq=2, Hkv=1, D=64, scale=0.0, dtype=0, dQ=A + 6 * SZ, dK=A + 7 * SZ, dV=A + 8 * SZ,
+             Hq=2, Hkv=1, D=64, scale=0.0, dtype=1, dQ=A + 6 * SZ, dK=A + 7 * SZ, dV=A + 8 * SZ,
              ws=A + 9 * SZ, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     L = _lib.lib()
@@ -137,7 +139,9 @@ def _bwd(**kw):
     (dict(LSE=A + 3 * SZ + 64), 1),        # LSE overlaps O
     (dict(ws=A + 2 * SZ + 32), 1),         # workspace overlaps V
     (dict(ws_bytes=16), 3),
+    (dict(ws_bytes=16, ws=A + 16), 3),     # too small is reported before overlap
     (dict(scale=float("nan")), 1),
+    (dict(dtype=0, ws=0, Q=0), 1),         # bf16: no workspace needed, other checks still apply
 ])
 def test_fwd_validation(kw, status):
     assert _fwd(**kw) == status

@@ -183,6 +183,8 @@ EDGE = [
     (2, 8, 2, 128, 256, 16),    # several full tiles, GQA 4
     (1, 4, 1, 64, 300, 64),     # ragged, large blocks
     (1, 2, 1, 128, 513, 3),     # several tiles + ragged tail
+    (1, 3, 1, 64, 100, 4),      # odd GQA ratio (the split walk halves are uneven)
+    (1, 6, 2, 128, 384, 8),     # GQA 3, several key tiles
 ]
 
 
@@ -268,8 +270,12 @@ def test_autograd_function():
 
 def test_workspace_too_small_raises_on_device():
     from paper_2512_22234_amd import BdAttnError
-    q, k, v, _ = (t.to(DEV) for t in make_random_case(1, 2, 1, 64, 64, 4, seed=17))
+    q, k, v, do = (t.to(DEV) for t in make_random_case(1, 2, 1, 64, 64, 4, seed=17))
+    o, lse = bd_attn_fwd(q, k, v, 64, 4)
     ws = torch.empty(64, dtype=torch.uint8, device=DEV)
     with pytest.raises(BdAttnError) as e:
-        bd_attn_fwd(q, k, v, 64, 4, workspace=ws)
+        bd_attn_bwd(do, q, k, v, o, lse, 64, 4, workspace=ws)
+    assert e.value.status == 3
+    with pytest.raises(BdAttnError) as e:
+        bd_attn_fwd(q.float(), k.float(), v.float(), 64, 4, workspace=ws)
     assert e.value.status == 3
