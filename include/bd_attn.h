@@ -112,9 +112,20 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
  * key tiles per query tile (forward and dQ, by_key_tile = 0) or query tiles
  * per key tile (dK/dV, by_key_tile = 1; that kernel repeats the walk for each
  * query head of the group).  A correct walk visits every non-EMPTY pair
- * exactly once.
+ * exactly once.  A visited pair whose class, as the kernels compute it
+ * without divisions, differs from bd_attn_classify_tiles_host's gets 64
+ * instead of 1.
  */
 int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out);
+
+/*
+ * Host-side copy of the per-element visibility rule of PARTIAL tiles
+ * (exposed for tests): the kernels test a position against a window
+ * [lo, hi) computed once per row.  Writes the 2L x 2L mask out[q*2L + k]
+ * (1 = visible) rebuilt from the windows of every query row (by_key = 0,
+ * forward and dQ) or of every key row (by_key = 1, dK/dV).
+ */
+int bd_attn_mask_windows_host(int L, int S, int by_key, int8_t* out);
 
 /*
  * Benchmark variants of bd_attn_fwd / bd_attn_bwd: identical work and

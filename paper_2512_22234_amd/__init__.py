@@ -24,7 +24,8 @@ BD_ATTN_FP32 = 1
 
 __all__ = [
     "bd_attn", "BdAttnFunction", "bd_attn_fwd", "bd_attn_bwd", "bd_attn_workspace_bytes",
-    "bd_attn_classify_tiles_host", "bd_attn_visit_lists_host", "bd_attn_status_string",
+    "bd_attn_classify_tiles_host", "bd_attn_visit_lists_host", "bd_attn_mask_windows_host",
+    "bd_attn_status_string",
     "bd_attn_version", "bd_attn_fwd_marked", "bd_attn_bwd_marked", "bd_attn_stage_names",
     "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
 ]
@@ -89,6 +90,14 @@ def bd_attn_visit_lists_host(L: int, S: int, BM: int, BN: int, by_key_tile: bool
     st = lib().bd_attn_visit_lists_host(L, S, BM, BN, int(by_key_tile), out.ctypes.data_as(ctypes.c_void_p))
     if st:
         raise BdAttnError(st, "bd_attn_visit_lists_host")
+    return out
+
+
+def bd_attn_mask_windows_host(L: int, S: int, by_key: bool) -> np.ndarray:
+    out = np.zeros((2 * L, 2 * L), dtype=np.int8)
+    st = lib().bd_attn_mask_windows_host(L, S, int(by_key), out.ctypes.data_as(ctypes.c_void_p))
+    if st:
+        raise BdAttnError(st, "bd_attn_mask_windows_host")
     return out
 
 

@@ -6,7 +6,7 @@
 
 #include <cmath>
 
-#include "../../include/bd_attn.h"
+#include "bd_attn.h"
 #include "kernels.hpp"
 #include "tiles.hpp"
 
@@ -17,7 +17,7 @@ constexpr int kVersion = 100;  // 0.1.0
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t delta = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
+  size_t delta = 0, lse2 = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
 };
 
 bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
@@ -31,6 +31,8 @@ Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
   size_t off = 0;
   if (bwd) {
     w.delta = off;
+    off += align256((size_t)B * Hq * N * 4);
+    w.lse2 = off;
     off += align256((size_t)B * Hq * N * 4);
     w.part = off;
     off += align256(bd::dkdv_partial_floats(B, Hkv, L, D) * 4);
@@ -158,22 +160,54 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
   memset(out, 0, (size_t)nq * nk);
   if (!by_key_tile) {
     for (int a = 0; a < nq; ++a) {
-      const bd::KeyTileList kl = bd::key_tiles_for_query_tile(a / nqt, a % nqt, L, S, BM, BN);
+      const int qh = a / nqt, q0 = (a % nqt) * BM, q1 = bd::imin(L, q0 + BM);
+      const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;
+      const bd::KeyTileList kl = bd::key_tiles_for_query_tile(qh, a % nqt, L, S, BM, BN);
       for (int t = 0; t < kl.count(); ++t) {
         int kh, j;
         kl.at(t, kh, j);
         if (j < 0 || j >= nkt) return BD_ATTN_ERR_INVALID_ARGUMENT;
-        out[(size_t)a * nk + kh * nkt + j] += 1;
+        const int k0 = j * BN, k1 = bd::imin(L, k0 + BN);
+        const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
+        const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
+        const int fast = bd::classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, full);
+        out[(size_t)a * nk + kh * nkt + j] += (int8_t)(fast == ref ? 1 : 64);
       }
     }
   } else {
     for (int c = 0; c < nk; ++c) {
-      const bd::QueryTileList ql = bd::query_tiles_for_key_tile(c / nkt, c % nkt, L, S, BM, BN);
+      const int kh = c / nkt, k0 = (c % nkt) * BN, k1 = bd::imin(L, k0 + BN);
+      const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
+      const bd::QueryTileList ql = bd::query_tiles_for_key_tile(kh, c % nkt, L, S, BM, BN);
       for (int t = 0; t < ql.count(); ++t) {
         int qh, i;
         ql.at(t, qh, i);
         if (i < 0 || i >= nqt) return BD_ATTN_ERR_INVALID_ARGUMENT;
-        out[(size_t)(qh * nqt + i) * nk + c] += 1;
+        const int q0 = i * BM, q1 = bd::imin(L, q0 + BM);
+        const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
+        const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
+        const int fast = bd::classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, full);
+        out[(size_t)(qh * nqt + i) * nk + c] += (int8_t)(fast == ref ? 1 : 64);
+      }
+    }
+  }
+  return BD_ATTN_OK;
+}
+
+int bd_attn_mask_windows_host(int L, int S, int by_key, int8_t* out) {
+  if (L < 1 || S < 1 || out == nullptr) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (S > L) S = L;
+  const int N = 2 * L;
+  memset(out, 0, (size_t)N * N);
+  for (int a = 0; a < N; ++a) {  // the row's own position
+    const int ah = a / L, ap = a % L, a0 = (ap / S) * S;
+    for (int oh = 0; oh < 2; ++oh) {  // the other side's half
+      const bd::PosWindow win = by_key ? bd::queries_seeing(ah, oh, a0, L, S, true)
+                                       : bd::keys_visible_from(ah, oh, a0, L, S, true);
+      for (int x = win.lo; x < win.hi; ++x) {
+        const int other = oh * L + x;
+        if (by_key) out[(size_t)other * N + a] = 1;  // query `other` sees key a
+        else out[(size_t)a * N + other] = 1;         // query a sees key `other`
       }
     }
   }
@@ -307,11 +341,12 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
     dv = wb + w.dv;
   }
   float* delta = reinterpret_cast<float*>(wb + w.delta);
-  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, delta, stream));
+  float* lse2 = reinterpret_cast<float*>(wb + w.lse2);
+  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, LSE, delta, lse2, stream));
   float* part = reinterpret_cast<float*>(wb + w.part);
-  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, LSE, delta, dk, dv, part, stream));
+  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, lse2, delta, dk, dv, part, stream));
   BD_LAUNCH(bd::launch_bwd_dkdv_combine(s, part, dk, dv, stream));
-  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, LSE, delta, dq, stream));
+  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, lse2, delta, dq, stream));
   if (dtype == BD_ATTN_FP32) {
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));

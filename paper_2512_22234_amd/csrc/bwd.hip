@@ -2,8 +2,8 @@
 // vector-Jacobian product of softmax attention under the mask of Eq. 1 / Eq. 2
 // (DiRL Section 4.1), with no atomics, so results are bitwise reproducible.
 //
-//   Delta = rowsum(dO * O)                              (bwd_pre)
-//   P     = exp(scale Q K^T - LSE) on visible pairs
+//   Delta = rowsum(dO * O), lse2 = LSE * log2(e)        (bwd_pre)
+//   P     = exp2(scale*log2(e) * Q K^T - lse2) on visible pairs
 //   dV    = P^T dO,  dP = dO V^T,  dS = P * (dP - Delta)
 //   dK    = scale dS^T Q                                (dkdv, key-tile major)
 //   dQ    = scale dS K                                  (dq, query-tile major)
@@ -13,16 +13,19 @@
 // heads of the GQA group and the 64-row query tiles that can see the key tile
 // (the exact tile classification gives the list).  Scores are S = Q K^T so
 // each lane owns one key column; P and dS are then directly the B operands of
-// dV^T = dO^T P and dK^T = Q^T dS, whose A operands come from the row-major Q
-// and dO tiles through the transposing LDS read.  Work per clean key tile
-// shrinks linearly with its position, so each clean tile's walk is split into
-// two halves run by two workgroups that write float32 partial sums; a combine
+// dV^T = dO^T P and dK^T = Q^T dS, whose A operands come from the Q and dO
+// tiles through the transposing LDS read.  Work per clean key tile shrinks
+// linearly with its position, so each clean tile's walk is split into two
+// halves run by two workgroups that write float32 partial sums; a combine
 // kernel adds the two halves in a fixed order.  Noisy key tiles (seen only by
 // their own block's noisy queries) are done by one workgroup each.
 //
 // dq: a workgroup owns a (batch, query head, 128-row query tile) like the
 // forward; scores are S^T = K Q^T (lane = query) and dQ^T = K^T dS^T with K^T
-// read from the row-major K tile through the transposing LDS read.
+// read from the K tile through the transposing LDS read.
+//
+// Tiles are copied into LDS asynchronously (global_load_lds) one step ahead,
+// double-buffered.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -30,11 +33,12 @@ namespace bd {
 namespace {
 
 // ----------------------------------------------------------------------------
-// Delta = rowsum(dO * O) in fp32; D/8 consecutive lanes share one row.
+// Delta = rowsum(dO * O) and lse2 = LSE * log2(e), fp32; D/8 consecutive lanes
+// share one row.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O,
-                                                      const bf16* __restrict__ dO,
-                                                      float* __restrict__ delta, size_t rows) {
+__global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O, const bf16* __restrict__ dO,
+                                                      const float* __restrict__ LSE, float* __restrict__ delta,
+                                                      float* __restrict__ lse2, size_t rows) {
   constexpr int TPR = D / 8;
   const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
   const size_t row = gid / TPR;
@@ -48,7 +52,10 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O
   }
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (row < rows && part == 0) delta[row] = acc;
+  if (row < rows && part == 0) {
+    delta[row] = acc;
+    lse2[row] = LSE[row] * LOG2E;
+  }
 }
 
 // ----------------------------------------------------------------------------
@@ -57,7 +64,7 @@ struct DkvParams {
   const bf16* K;
   const bf16* V;
   const bf16* dO;
-  const float* LSE;
+  const float* lse2;
   const float* delta;
   bf16* dK;
   bf16* dV;
@@ -70,22 +77,56 @@ struct DkvParams {
 template <int D>
 struct DkvSmem {
   static constexpr int BM = DKV_BM;
-  static constexpr int QS = D + 8;  // row stride (elements)
-  bf16 q[2][BM * QS];
-  bf16 dO[2][BM * QS];
+  static constexpr uint32_t TILE = BM * D * 2;  // bytes per swizzled tile
+  bf16 q[2][BM * D];   // byte offset buf * TILE
+  bf16 dO[2][BM * D];  // byte offset (2 + buf) * TILE
   alignas(16) float lse2[2][BM];
   alignas(16) float dlt[2][BM];
-  alignas(16) int qblk[2][BM];
+};
+
+// dK/dV accumulation.  PIN keeps the accumulators in AGPRs through inline-asm
+// MFMAs (no per-iteration register copies); it is used only where the
+// compiler leaves those registers in place across the loop (D = 128; a CPU
+// test inspects the generated code), since a copy of an asm-defined
+// accumulator would not be padded for the MFMA latency.  Otherwise the
+// builtin, whose hazards the compiler tracks.
+template <bool PIN>
+__device__ inline f32x16 acc_zero() {
+  if constexpr (PIN) return mfma32_agpr_zero();
+  f32x16 z;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) z[e] = 0.f;
+  return z;
+}
+template <bool PIN>
+__device__ inline void acc_mfma(f32x16& acc, const bf16x8& a, const bf16x8& b, bool fresh) {
+  if constexpr (PIN) {
+    if (fresh) mfma32_agpr<true>(acc, a, b);
+    else mfma32_agpr<false>(acc, a, b);
+  } else {
+    acc = mfma32(a, b, acc);
+  }
+}
+
+// Position in a head-major walk over (query head g, query tile u).
+struct WalkPos {
+  int g, u;
+  __device__ void next(int per_g) {
+    if (++u == per_g) {
+      u = 0;
+      ++g;
+    }
+  }
 };
 
 template <int D>
 __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   constexpr int BM = DKV_BM, BN = DKV_BN;
-  constexpr int DS = D / 16, DB = D / 32, QB = BM / 32, PC = BM / 16;
-  constexpr int QS = DkvSmem<D>::QS;
-  constexpr int NCH = BM * D / 8 / 256;  // 16-byte chunks per thread, for each of Q and dO
-  static_assert(NCH * 256 * 8 == BM * D, "tile must split evenly over 256 threads");
+  constexpr int DS = D / 16, DB = D / 32, QB = BM / 32;
+  constexpr bool PIN = D == 128;
+  constexpr uint32_t TILE = DkvSmem<D>::TILE;
   __shared__ DkvSmem<D> sm;
+  char* lds = reinterpret_cast<char*>(&sm);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
@@ -103,11 +144,37 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int split = clean ? (rank & 1) : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
   const int k0 = j * BN, k1 = imin(L, k0 + BN);
+  const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
 
   const int kk = k0 + w * 32 + l32;  // this lane's key (local to its half)
   const bool kvalid = kk < k1;
-  const int bk = kvalid ? kk / S : KBLK_INVALID;
+  const int kblock0 = kvalid ? (kk / S) * S : 0;
   const size_t krow = (size_t)grp * N + kh * L + kk;
+
+  const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
+  const int per_g = ql.count();
+  const int Tall = p.G * per_g;
+  const int t0 = clean ? (split * Tall) / 2 : 0;
+  const int t1 = clean ? ((split + 1) * Tall) / 2 : Tall;
+  const int T = t1 - t0;
+
+  const TileCopy<D, BM, 256> copy(tid);
+  auto issue = [&](WalkPos wp, int buf) {
+    int qh, i;
+    ql.at(wp.u, qh, i);
+    const size_t row0 = ((size_t)b * p.Hq + hk * p.G + wp.g) * N + qh * L;  // first row of the half
+    copy.issue(p.Q + row0 * D, i * BM, L, lds, buf * TILE, tid);
+    copy.issue(p.dO + row0 * D, i * BM, L, lds, (2 + buf) * TILE, tid);
+    if (w == 0) async_load_row_floats(p.lse2 + row0, i * BM, L, sm.lse2[buf], lane);
+    if (w == 1) async_load_row_floats(p.delta + row0, i * BM, L, sm.dlt[buf], lane);
+  };
+  WalkPos cur = {0, 0};
+  if (per_g > 0) cur = {t0 / per_g, t0 % per_g};
+  WalkPos nxt = cur;
+  if (T > 0) {
+    issue(cur, 0);
+    nxt.next(per_g);
+  }
 
   bf16x8 kreg[DS], vreg[DS];
 #pragma unroll
@@ -116,136 +183,83 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
     vreg[s] = kvalid ? *reinterpret_cast<const bf16x8*>(p.V + krow * D + 16 * s + 8 * g2) : zero_bf16x8();
   }
 
-  const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
-  const int per_g = ql.count();
-  const int Tall = p.G * per_g;
-  const int t0 = clean ? (split * Tall) / 2 : 0;
-  const int t1 = clean ? ((split + 1) * Tall) / 2 : Tall;
-
-  u32x4 qst[NCH], dost[NCH];
-  float lse_st = 0.f, dlt_st = 0.f;
-  int qb_st = QBLK_INVALID;
-  auto load_tile = [&](int t) {
-    const int g = t / per_g;
-    int qh, i;
-    ql.at(t - g * per_g, qh, i);
-    const size_t bhq = (size_t)b * p.Hq + hk * p.G + g;
-    const size_t hbase = (bhq * N + qh * L) * D;
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      qst[u] = ld16_rows(p.Q + hbase, i * BM + row, L, D, col8 * 8);
-      dost[u] = ld16_rows(p.dO + hbase, i * BM + row, L, D, col8 * 8);
-    }
-    if (tid < BM) {
-      const int qr = i * BM + tid;
-      const bool ok = qr < L;
-      const size_t rr = bhq * N + qh * L + (ok ? qr : L - 1);
-      lse_st = p.LSE[rr];  // rows past the end are masked (qblk invalid)
-      dlt_st = p.delta[rr];
-      qb_st = ok ? qr / S : QBLK_INVALID;
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      st16(&sm.q[buf][row * QS + col8 * 8], qst[u]);
-      st16(&sm.dO[buf][row * QS + col8 * 8], dost[u]);
-    }
-    if (tid < BM) {
-      sm.lse2[buf][tid] = lse_st * LOG2E;
-      sm.dlt[buf][tid] = dlt_st;
-      sm.qblk[buf][tid] = qb_st;
-    }
-  };
-
+  const LdsOperands<D> ops(lane);
   f32x16 dkacc[DB], dvacc[DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      dkacc[db][e] = 0.f;
-      dvacc[db][e] = 0.f;
-    }
-
-  if (t0 < t1) {
-    load_tile(t0);
-    store_tile(0);
+  for (int db = 0; db < DB; ++db) {
+    dkacc[db] = acc_zero<PIN>();
+    dvacc[db] = acc_zero<PIN>();
   }
-  wait_global_loads();  // K/V rows are in registers; the loop only waits on its own prefetch
+
+  wait_global_loads();
   __syncthreads();
 
-  for (int t = t0; t < t1; ++t) {
-    const int buf = (t - t0) & 1;
-    if (t + 1 < t1) load_tile(t + 1);
-    const int g = t / per_g;
+  for (int t = 0; t < T; ++t) {
+    const int buf = t & 1;
+    const uint32_t qrb = buf * TILE + ops.row_rel, drb = (2 + buf) * TILE + ops.row_rel;
+    const uint32_t qt0 = buf * TILE + ops.tr_rel0, qt1 = buf * TILE + ops.tr_rel1;
+    const uint32_t dt0 = (2 + buf) * TILE + ops.tr_rel0, dt1 = (2 + buf) * TILE + ops.tr_rel1;
+    if (t + 1 < T) {
+      issue(nxt, buf ^ 1);
+      nxt.next(per_g);
+    }
     int qh, i;
-    ql.at(t - g * per_g, qh, i);
+    ql.at(cur.u, qh, i);
+    cur.next(per_g);
     const int q0 = i * BM, q1 = imin(L, q0 + BM);
-    const int cls = classify_pair(qh, q0, q1, kh, k0, k1, S, (q1 - q0) == BM && (k1 - k0) == BN);
+    const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
     if (cls != TILE_EMPTY) {
-      f32x16 sacc[QB], dpacc[QB];
+      // query q0 + offset sees this lane's key iff win.lo <= q0 + offset < win.hi
+      const PosWindow win = queries_seeing(kh, qh, kblock0, L, S, kvalid);
+      const unsigned span = cls == TILE_PARTIAL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
+      const int rel = cls == TILE_PARTIAL ? q0 + 4 * g2 - win.lo : 0;
+      // one 32-query block at a time keeps S, dP, P and dS of a single block live
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x16 sacc, dpacc;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          sacc[qb][e] = 0.f;
-          dpacc[qb][e] = 0.f;
+          sacc[e] = 0.f;
+          dpacc[e] = 0.f;
         }
-      // S[q][key] = sum_d Q[q][d] K[key][d];  dP[q][key] = sum_d dO[q][d] V[key][d]
+        // S[q][key] = sum_d Q[q][d] K[key][d];  dP[q][key] = sum_d dO[q][d] V[key][d]
 #pragma unroll
-      for (int s = 0; s < DS; ++s)
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          const bf16x8 aq = lds_bf16x8(&sm.q[buf][(qb * 32 + l32) * QS + 16 * s + 8 * g2]);
-          sacc[qb] = mfma32(aq, kreg[s], sacc[qb]);
-          const bf16x8 ad = lds_bf16x8(&sm.dO[buf][(qb * 32 + l32) * QS + 16 * s + 8 * g2]);
-          dpacc[qb] = mfma32(ad, vreg[s], dpacc[qb]);
+        for (int s = 0; s < DS; ++s) {
+          sacc = mfma32(lds_rows<D>(lds, qrb, s, qb), kreg[s], sacc);
+          dpacc = mfma32(lds_rows<D>(lds, drb, s, qb), vreg[s], dpacc);
         }
-      const bool partial = cls == TILE_PARTIAL;
-      const BlockWindow win = query_window(qh, kh, bk);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int i4 = 0; i4 < 4; ++i4) {
           const int rr = qb * 32 + 8 * i4 + 4 * g2;
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sm.lse2[buf][rr]);
           const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sm.dlt[buf][rr]);
-          const int4 qb4 = *reinterpret_cast<const int4*>(&sm.qblk[buf][rr]);
-          const int qbv[4] = {qb4.x, qb4.y, qb4.z, qb4.w};
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
-            float pv = fast_exp2(sacc[qb][4 * i4 + jj] * p.c - l4[jj]);
-            pv = (!partial || win.has(qbv[jj])) ? pv : 0.f;
-            dpacc[qb][4 * i4 + jj] = pv * (dpacc[qb][4 * i4 + jj] - d4[jj]);
-            sacc[qb][4 * i4 + jj] = pv;
+            float pv = fast_exp2(sacc[4 * i4 + jj] * p.c - l4[jj]);
+            pv = (unsigned)(rel + qb * 32 + 8 * i4 + jj) < span ? pv : 0.f;
+            dpacc[4 * i4 + jj] = pv * (dpacc[4 * i4 + jj] - d4[jj]);
+            sacc[4 * i4 + jj] = pv;
           }
         }
-      bf16x8 pb[PC], dsb[PC];
+        // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]
 #pragma unroll
-      for (int c = 0; c < PC; ++c) {
-        pb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
-        dsb[c] = pack8(dpacc[c >> 1], 8 * (c & 1));
-      }
-      // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]
+        for (int h = 0; h < 2; ++h) {
+          const bf16x8 pb = pack8(sacc, 8 * h), dsb = pack8(dpacc, 8 * h);
+          const int c = 2 * qb + h;
 #pragma unroll
-      for (int c = 0; c < PC; ++c)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16x8 ad = lds_read_tr(sm.dO[buf], QS, 16 * c, db * 32, lane);
-          dvacc[db] = mfma32(ad, pb[c], dvacc[db]);
-          const bf16x8 aq = lds_read_tr(sm.q[buf], QS, 16 * c, db * 32, lane);
-          dkacc[db] = mfma32(aq, dsb[c], dkacc[db]);
+          for (int db = 0; db < DB; ++db) {
+            acc_mfma<PIN>(dvacc[db], lds_tr<D>(lds, dt0, dt1, c, db), pb, db == 0);
+            acc_mfma<PIN>(dkacc[db], lds_tr<D>(lds, qt0, qt1, c, db), dsb, db == 0);
+          }
         }
+      }
     }
     compute_fence();
-    if (t + 1 < t1) store_tile(buf ^ 1);
+    wait_global_loads();
     __syncthreads();
   }
 
+  if constexpr (PIN) mfma_drain(dkacc, dvacc);
   if (!kvalid) return;
   const float sc = p.scale;
   if (clean) {
@@ -305,7 +319,7 @@ struct DqParams {
   const bf16* K;
   const bf16* V;
   const bf16* dO;
-  const float* LSE;
+  const float* lse2;
   const float* delta;
   bf16* dQ;
   int L, S, Hq, Hkv, G, nQT, nbh;
@@ -316,20 +330,18 @@ struct DqParams {
 template <int D>
 struct DqSmem {
   static constexpr int BN = DQ_BN;
-  static constexpr int KS = D + 8;
-  bf16 k[2][BN * KS];
-  bf16 v[2][BN * KS];
-  alignas(16) int kblk[2][BN];
+  static constexpr uint32_t TILE = BN * D * 2;  // bytes per swizzled tile
+  bf16 k[2][BN * D];  // byte offset buf * TILE
+  bf16 v[2][BN * D];  // byte offset (2 + buf) * TILE
 };
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   constexpr int BM = DQ_BM, BN = DQ_BN;
   constexpr int DS = D / 16, DB = D / 32, KB = BN / 32, PC = BN / 16;
-  constexpr int KS = DqSmem<D>::KS;
-  constexpr int NCH = BN * D / 8 / 256;
-  static_assert(NCH * 256 * 8 == BN * D, "tile must split evenly over 256 threads");
+  constexpr uint32_t TILE = DqSmem<D>::TILE;
   __shared__ DqSmem<D> sm;
+  char* lds = reinterpret_cast<char*>(&sm);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
@@ -342,14 +354,27 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
+  const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;
 
   const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
 
   const int r = q0 + w * 32 + l32;
   const bool qvalid = r < q1;
-  const int bq = qvalid ? r / S : QBLK_INVALID;
+  const int qblock0 = qvalid ? (r / S) * S : 0;
   const int prow = qh * L + r;
   const size_t qrow = (size_t)bh * N + prow;
+
+  const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
+  const int T = kl.count();
+  const TileCopy<D, BN, 256> copy(tid);
+  auto issue = [&](int t) {
+    int kh, j;
+    kl.at(t, kh, j);
+    const size_t hb = kvbase + (size_t)kh * L * D;
+    copy.issue(p.K + hb, j * BN, L, lds, (t & 1) * TILE, tid);
+    copy.issue(p.V + hb, j * BN, L, lds, (2 + (t & 1)) * TILE, tid);
+  };
+  if (T > 0) issue(0);
 
   bf16x8 qreg[DS], doreg[DS];
 #pragma unroll
@@ -357,62 +382,28 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     qreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.Q + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
     doreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.dO + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
   }
-  const float lse2 = qvalid ? p.LSE[qrow] * LOG2E : 0.f;
+  const float lse2 = qvalid ? p.lse2[qrow] : 0.f;
   const float dlt = qvalid ? p.delta[qrow] : 0.f;
 
-  const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
-  const int T = kl.count();
-
-  u32x4 kst[NCH], vst[NCH];
-  int kbst = 0;
-  auto load_tile = [&](int t) {
-    int kh, j;
-    kl.at(t, kh, j);
-    const bf16* kp = p.K + kvbase + (size_t)kh * L * D;
-    const bf16* vp = p.V + kvbase + (size_t)kh * L * D;
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      kst[u] = ld16_rows(kp, j * BN + row, L, D, col8 * 8);
-      vst[u] = ld16_rows(vp, j * BN + row, L, D, col8 * 8);
-    }
-    if (tid < BN) {
-      const int key = j * BN + tid;
-      kbst = key < L ? key / S : KBLK_INVALID;
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      st16(&sm.k[buf][row * KS + col8 * 8], kst[u]);
-      st16(&sm.v[buf][row * KS + col8 * 8], vst[u]);
-    }
-    if (tid < BN) sm.kblk[buf][tid] = kbst;
-  };
-
+  const LdsOperands<D> ops(lane);
   f32x16 dqacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dqacc[db][e] = 0.f;
 
-  if (T > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  wait_global_loads();  // Q/dO rows are in registers; the loop only waits on its own prefetch
+  wait_global_loads();
   __syncthreads();
 
   for (int t = 0; t < T; ++t) {
     const int buf = t & 1;
-    if (t + 1 < T) load_tile(t + 1);
+    const uint32_t krb = buf * TILE + ops.row_rel, vrb = (2 + buf) * TILE + ops.row_rel;
+    const uint32_t kt0 = buf * TILE + ops.tr_rel0, kt1 = buf * TILE + ops.tr_rel1;
+    if (t + 1 < T) issue(t + 1);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
-    const int cls = classify_pair(qh, q0, q1, kh, k0, k1, S, (q1 - q0) == BM && (k1 - k0) == BN);
+    const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
     if (cls != TILE_EMPTY) {
       f32x16 sacc[KB], dpacc[KB];
 #pragma unroll
@@ -427,27 +418,23 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       for (int s = 0; s < DS; ++s)
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
-          const bf16x8 ak = lds_bf16x8(&sm.k[buf][(kb * 32 + l32) * KS + 16 * s + 8 * g2]);
-          sacc[kb] = mfma32(ak, qreg[s], sacc[kb]);
-          const bf16x8 av = lds_bf16x8(&sm.v[buf][(kb * 32 + l32) * KS + 16 * s + 8 * g2]);
-          dpacc[kb] = mfma32(av, doreg[s], dpacc[kb]);
+          sacc[kb] = mfma32(lds_rows<D>(lds, krb, s, kb), qreg[s], sacc[kb]);
+          dpacc[kb] = mfma32(lds_rows<D>(lds, vrb, s, kb), doreg[s], dpacc[kb]);
         }
-      const bool partial = cls == TILE_PARTIAL;
-      const BlockWindow win = key_window(qh, kh, bq);
+      const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
+      const unsigned span = cls == TILE_PARTIAL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
+      const int rel = cls == TILE_PARTIAL ? k0 + 4 * g2 - win.lo : 0;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int4 kb4 = *reinterpret_cast<const int4*>(&sm.kblk[buf][kb * 32 + 8 * i + 4 * g2]);
-          const int kbv[4] = {kb4.x, kb4.y, kb4.z, kb4.w};
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             const int e = 4 * i + jj;
             float pv = fast_exp2(sacc[kb][e] * p.c - lse2);
-            pv = (!partial || win.has(kbv[jj])) ? pv : 0.f;
+            pv = (unsigned)(rel + kb * 32 + 8 * i + jj) < span ? pv : 0.f;
             sacc[kb][e] = pv * (dpacc[kb][e] - dlt);
           }
-        }
       bf16x8 dsb[PC];
 #pragma unroll
       for (int c = 0; c < PC; ++c) dsb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
@@ -455,13 +442,10 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 #pragma unroll
       for (int c = 0; c < PC; ++c)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16x8 a = lds_read_tr(sm.k[buf], KS, 16 * c, db * 32, lane);
-          dqacc[db] = mfma32(a, dsb[c], dqacc[db]);
-        }
+        for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(lds, kt0, kt1, c, db), dsb[c], dqacc[db]);
     }
     compute_fence();
-    if (t + 1 < T) store_tile(buf ^ 1);
+    wait_global_loads();
     __syncthreads();
   }
 
@@ -478,24 +462,25 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 }
 
 template <int D>
-hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, float* delta, hipStream_t st) {
+hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, const float* LSE, float* delta,
+                        float* lse2, hipStream_t st) {
   const size_t rows = (size_t)s.B * s.Hq * 2 * s.L;
   const size_t threads = rows * (D / 8);
   const dim3 grid((unsigned)((threads + 255) / 256));
   hipLaunchKernelGGL(bwd_pre_kernel<D>, grid, dim3(256), 0, st, static_cast<const bf16*>(O),
-                     static_cast<const bf16*>(dO), delta, rows);
+                     static_cast<const bf16*>(dO), LSE, delta, lse2, rows);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* LSE, const float* delta, void* dK, void* dV, float* part, hipStream_t st) {
+                         const float* lse2, const float* delta, void* dK, void* dV, float* part, hipStream_t st) {
   DkvParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
-  p.LSE = LSE;
+  p.lse2 = lse2;
   p.delta = delta;
   p.dK = static_cast<bf16*>(dK);
   p.dV = static_cast<bf16*>(dV);
@@ -516,13 +501,13 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
 
 template <int D>
 hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                       const float* LSE, const float* delta, void* dQ, hipStream_t st) {
+                       const float* lse2, const float* delta, void* dQ, hipStream_t st) {
   DqParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
-  p.LSE = LSE;
+  p.lse2 = lse2;
   p.delta = delta;
   p.dQ = static_cast<bf16*>(dQ);
   p.L = s.L;
@@ -541,16 +526,17 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
 
 }  // namespace
 
-hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, float* delta, hipStream_t st) {
-  if (s.D == 128) return launch_pre_d<128>(s, O, dO, delta, st);
-  return launch_pre_d<64>(s, O, dO, delta, st);
+hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, const float* LSE, float* delta,
+                          float* lse2, hipStream_t st) {
+  if (s.D == 128) return launch_pre_d<128>(s, O, dO, LSE, delta, lse2, st);
+  return launch_pre_d<64>(s, O, dO, LSE, delta, lse2, st);
 }
 
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                           const float* LSE, const float* delta, void* dK, void* dV, float* part,
+                           const float* lse2, const float* delta, void* dK, void* dV, float* part,
                            hipStream_t st) {
-  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, LSE, delta, dK, dV, part, st);
-  return launch_dkdv_d<64>(s, Q, K, V, dO, LSE, delta, dK, dV, part, st);
+  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, lse2, delta, dK, dV, part, st);
+  return launch_dkdv_d<64>(s, Q, K, V, dO, lse2, delta, dK, dV, part, st);
 }
 
 hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, void* dV, hipStream_t st) {
@@ -564,9 +550,9 @@ hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, 
 }
 
 hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* LSE, const float* delta, void* dQ, hipStream_t st) {
-  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, LSE, delta, dQ, st);
-  return launch_dq_d<64>(s, Q, K, V, dO, LSE, delta, dQ, st);
+                         const float* lse2, const float* delta, void* dQ, hipStream_t st) {
+  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, lse2, delta, dQ, st);
+  return launch_dq_d<64>(s, Q, K, V, dO, lse2, delta, dQ, st);
 }
 
 }  // namespace bd

@@ -28,34 +28,97 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
-constexpr int KBLK_INVALID = 0x3fffffff;  // block index of a key past the end of its half
-constexpr int QBLK_INVALID = -1;          // block index of a query past the end of its half
+
+__device__ inline bf16x8 zero_bf16x8() {
+  u32x4 z = {0u, 0u, 0u, 0u};
+  return __builtin_bit_cast(bf16x8, z);
+}
 
 __device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+
+// The same MFMA with its accumulator pinned to AGPRs (the "+a" constraint).
+// For long-lived accumulators that only MFMAs touch inside a loop: it keeps
+// the register allocator from parking them in AGPRs between iterations and
+// copying them through VGPRs on every pass.  The compiler's hazard tracking
+// does not see inside the asm, so the two waits it would insert are explicit:
+//  - a VALU result feeding the MFMA as A or B needs two wait states; FRESH
+//    adds them (use it for the first MFMA after the operands are computed);
+//  - results must not be read by other instructions until mfma_drain() has
+//    run on every accumulator (it ties them as operands, so no read can be
+//    scheduled above it).
+// Back-to-back accumulation into the same registers needs no wait states.
+template <bool FRESH = false>
+__device__ inline void mfma32_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  if constexpr (FRESH)
+    asm volatile("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// A zero accumulator defined directly in AGPRs (an MFMA of zero operands), so
+// that every definition and loop use of an mfma32_agpr accumulator is AGPR.
+__device__ inline f32x16 mfma32_agpr_zero() {
+  f32x16 acc;
+  const bf16x8 z = zero_bf16x8();
+  asm volatile("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
+  return acc;
+}
+// 64 wait states, more than the write latency of an 8-pass MFMA, with the
+// accumulators of two arrays tied as operands so that every later read of
+// them is ordered after the wait.
+#define BD_MFMA_DRAIN_NOPS "s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7"
+template <int N>
+__device__ inline void mfma_drain(f32x16 (&x)[N], f32x16 (&y)[N]) {
+  static_assert(N == 2 || N == 4, "two or four accumulators per array");
+  if constexpr (N == 4)
+    asm volatile(BD_MFMA_DRAIN_NOPS
+                 : "+a"(x[0]), "+a"(x[1]), "+a"(x[2]), "+a"(x[3]), "+a"(y[0]), "+a"(y[1]), "+a"(y[2]), "+a"(y[3]));
+  else
+    asm volatile(BD_MFMA_DRAIN_NOPS : "+a"(x[0]), "+a"(x[1]), "+a"(y[0]), "+a"(y[1]));
+}
+#undef BD_MFMA_DRAIN_NOPS
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-// MFMA A/B operand for a contraction over the ROW index of a row-major LDS
-// tile X[row][col] (row stride `stride` elements): returns, for this lane, the
-// 8 values X[row0 + keyof(8*g + e)][col0 + l%32], e = 0..7, g = lane/32 -- the
-// operand layout described above with rows as contraction indices.
+// LDS tiles are row-major [rows][D] with no padding; the 16-byte chunks of a
+// row are permuted by an XOR with chunk_swizzle<D>(row).  With 64 four-byte
+// banks, the mask makes both access patterns below conflict-free for every
+// group of 16 lanes: 16-byte row slices of 16 consecutive rows at one column
+// (row-major MFMA operands), and 8-byte pieces of 4 consecutive rows x 32
+// bytes (the transposing read).  Padding can only fix one of the two.
+template <int D> __host__ __device__ inline int chunk_swizzle(int r);
+template <> __host__ __device__ inline int chunk_swizzle<128>(int r) {
+  return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+}
+template <> __host__ __device__ inline int chunk_swizzle<64>(int r) {
+  return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+}
+// Element index of (row, col) in a swizzled tile; col % 8 stays in place.
+template <int D> __host__ __device__ inline int tile_idx(int row, int col) {
+  return row * D + ((((col >> 3) ^ chunk_swizzle<D>(row)) << 3) | (col & 7));
+}
+
+// MFMA A/B operand for a contraction over the ROW index of a swizzled LDS
+// tile X[row][col]: returns, for this lane, the 8 values
+// X[row0 + keyof(8*g + e)][col0 + l%32], e = 0..7, g = lane/32 -- the operand
+// layout described above with rows as contraction indices.
 //
 // ds_read_b64_tr_b16 works on groups of 16 lanes: lane i of a group receives
 // element i%4 of the 8-byte chunks addressed by lanes 4r + i/4 of its group,
 // r = 0..3.  So lane 4r + c of a group points at row (base + r), columns
 // [4c, 4c+4) of its 16-column slice, and two reads cover rows keyof(0..3) and
 // keyof(4..7) of the lane's half-wave.
-__device__ inline bf16x8 lds_read_tr(const bf16* tile, int stride, int row0, int col0, int lane) {
+template <int D>
+__device__ inline bf16x8 lds_read_tr(const bf16* tile, int row0, int col0, int lane) {
   const int h = lane >> 4, j = lane & 15;
   const int row = row0 + 4 * (h >> 1) + (j >> 2);
   const int col = col0 + 16 * (h & 1) + 4 * (j & 3);
-  const bf16* p0 = tile + row * stride + col;
-  const bf16* p1 = p0 + 8 * stride;
+  const bf16* p0 = tile + tile_idx<D>(row, col);
+  const bf16* p1 = tile + tile_idx<D>(row + 8, col);
   const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p0));
   const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p1));
   typedef short s16x8 __attribute__((ext_vector_type(8)));
@@ -63,23 +126,121 @@ __device__ inline bf16x8 lds_read_tr(const bf16* tile, int stride, int row0, int
   return __builtin_bit_cast(bf16x8, v);
 }
 
-__device__ inline bf16x8 zero_bf16x8() {
-  u32x4 z = {0u, 0u, 0u, 0u};
-  return __builtin_bit_cast(bf16x8, z);
+// Per-lane byte offsets that turn every MFMA-operand read of a swizzled tile
+// into one XOR with a compile-time constant plus an immediate offset.  With
+// F = chunk_swizzle(row) depending only on row % 16, the chunk of a row-slice
+// read is (2s + g) ^ F, whose byte offset 32*(s ^ F/2) + 16*(g ^ F%2) equals
+// (32*F/2 + 16*(g ^ F%2)) ^ 32*s; likewise the feature block db of a
+// transposing read only flips bits 6-7.  Tile offsets must be multiples of
+// 256 bytes so that adding them leaves bits 0-7 alone.
+template <int D>
+struct LdsOperands {
+  uint32_t row_rel;          // row-slice reads: row 32*rb + lane%32, columns 16*s + 8*(lane/32)
+  uint32_t tr_rel0, tr_rel1;  // transposing reads (rows keyof(0..3) and keyof(4..7) of a chunk)
+  __device__ explicit LdsOperands(int lane) {
+    const int l32 = lane & 31, g = lane >> 5;
+    const int F = chunk_swizzle<D>(l32);
+    row_rel = (uint32_t)(l32 * 2 * D + 16 * (g ^ (F & 1)) + 32 * (F >> 1));
+    const int h = lane >> 4, j = lane & 15;
+    const int x = 2 * (h & 1) + ((j >> 1) & 1);
+    const int r0 = 4 * (h >> 1) + (j >> 2);
+    const int f0 = chunk_swizzle<D>(r0), f1 = chunk_swizzle<D>(r0 + 8);
+    constexpr int HI = (D / 8 - 1) & ~3;
+    tr_rel0 = (uint32_t)(r0 * 2 * D + 16 * (f0 & HI) + 16 * (x ^ (f0 & 3)) + 8 * (j & 1));
+    tr_rel1 = (uint32_t)((r0 + 8) * 2 * D + 16 * (f1 & HI) + 16 * (x ^ (f1 & 3)) + 8 * (j & 1));
+  }
+};
+
+// Row-slice operand (same values as lds_row8<D>(tile, 32*rb + lane%32, 16*s + 8*(lane/32)))
+// from a tile starting at byte offset `base - row_rel` of lds.
+template <int D>
+__device__ inline bf16x8 lds_rows(const char* lds, uint32_t base, int s, int rb) {
+  return *reinterpret_cast<const bf16x8*>(lds + ((base ^ (uint32_t)(32 * s)) + (uint32_t)(rb * 64 * D)));
 }
+// Transposing operand (same values as lds_read_tr<D>(tile, 16*c, 32*db, lane)); b0/b1 = tile offset + tr_rel0/1.
+template <int D>
+__device__ inline bf16x8 lds_tr(const char* lds, uint32_t b0, uint32_t b1, int c, int db) {
+  const uint32_t o = (uint32_t)(c * 32 * D);
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds + ((b0 ^ (uint32_t)(64 * db)) + o)));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(lds + ((b1 ^ (uint32_t)(64 * db)) + o)));
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Per-lane element offsets of the chunks a lane copies in async_load_tile
+// (they do not depend on which tile is copied).
+template <int D, int NR, int NT>
+struct TileCopy {
+  static constexpr int CPR = D / 8;
+  static constexpr int NW = NT / 64;
+  static constexpr int NI = NR * CPR / NT;
+  static_assert(NI * NT == NR * CPR, "tile must split evenly over the workgroup");
+  int goff[NI];  // element offset of the source chunk relative to the tile's first row
+  __device__ explicit TileCopy(int tid) {
+    const int w = tid >> 6, lane = tid & 63;
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int p = (u * NW + w) * 64 + lane;
+      const int row = p / CPR;
+      goff[u] = row * D + (((p % CPR) ^ chunk_swizzle<D>(row)) << 3);
+    }
+  }
+  // Copy rows [row0, row0 + NR) of src (clamped to < nrows) into the tile at
+  // LDS byte offset tile_off of lds (a multiple of 1 KiB).
+  __device__ void issue(const bf16* src, int row0, int nrows, char* lds, uint32_t tile_off, int tid) const {
+    const int w = tid >> 6;
+    const bool whole = row0 + NR <= nrows;
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      int off = row0 * D + goff[u];
+      if (!whole) {
+        const int row = goff[u] / D;
+        off = imin(row0 + row, nrows - 1) * D + (goff[u] - row * D);
+      }
+      __builtin_amdgcn_global_load_lds(src + off,
+                                       (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + w) * 1024),
+                                       16, 0, 0);
+    }
+  }
+};
+
+// Asynchronous copy of NR rows starting at row0 of a row-major bf16 array
+// [nrows][D] into a swizzled LDS tile [NR][D] (global_load_lds_dwordx4).  Each
+// wave instruction fills 1 KiB of LDS contiguously, 16 bytes per lane in lane
+// order; lane i fetches the global chunk that belongs at LDS chunk p (the XOR
+// swizzle is its own inverse).  Rows past nrows are clamped to the last row:
+// the kernels mask them out, so they only need finite data.  Completion is
+// tracked by the wave's vmcnt (wait_global_loads) and must be followed by a
+// workgroup barrier before other waves read the tile.
+template <int D, int NR, int NT>
+__device__ inline void async_load_tile(const bf16* src, int row0, int nrows, bf16* tile, int tid) {
+  constexpr int CPR = D / 8;            // 16-byte chunks per row
+  constexpr int NW = NT / 64;           // waves in the workgroup
+  constexpr int NI = NR * CPR / NT;     // instructions per wave
+  static_assert(NI * NT == NR * CPR, "tile must split evenly over the workgroup");
+  const int w = tid >> 6, lane = tid & 63;
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int blk = u * NW + w;         // 1 KiB block of the tile filled by this instruction
+    const int p = blk * 64 + lane;      // LDS chunk written by this lane
+    const int row = p / CPR;
+    const int chunk = (p % CPR) ^ chunk_swizzle<D>(row);
+    const int r = imin(row0 + row, nrows - 1);
+    __builtin_amdgcn_global_load_lds(src + (size_t)r * D + chunk * 8,
+                                     (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
+  }
+}
+
+// Asynchronous copy of 64 consecutive floats src[row0 .. row0+63] (indices
+// clamped to < nrows) into LDS dst[0..63]: one instruction of one wave.
+__device__ inline void async_load_row_floats(const float* src, int row0, int nrows, float* dst, int lane) {
+  const int r = imin(row0 + lane, nrows - 1);
+  __builtin_amdgcn_global_load_lds(src + r, (__attribute__((address_space(3))) void*)dst, 4, 0, 0);
+}
+
 
 __device__ inline u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
-
-// 16 bytes of row min(row, nrows-1) of a row-major bf16 array.  Rows past the
-// end of a half are always masked out of the softmax (their P is exactly 0),
-// so they only need to hold finite data; clamping keeps the load
-// unconditional and its result unused until the LDS store, so the compiler's
-// count of outstanding loads stays exact and the load latency overlaps the
-// compute of the current tile.
-__device__ inline u32x4 ld16_rows(const bf16* base, int row, int nrows, int row_elems, int col) {
-  const int r = row < nrows ? row : nrows - 1;
-  return ld16(base + (size_t)r * row_elems + col);
-}
 
 // Keeps the compiler from moving memory operations or scheduling instructions
 // across this point.  Placed between a tile's compute and the LDS stores of
@@ -93,25 +254,13 @@ __device__ inline void compute_fence() {
 // Wait until every global load this wave issued has landed (s_waitcnt vmcnt(0)).
 __device__ inline void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Block-index window [lo, hi] of keys visible from one query (block bq, or
-// QBLK_INVALID past the end of its half) in the quadrant (qh, kh); an empty
-// window has lo > hi.  Keys past the end carry KBLK_INVALID and never fall in.
-struct BlockWindow {
-  int lo, hi;
-  __device__ bool has(int b) const { return b >= lo && b <= hi; }
-};
-__device__ inline BlockWindow key_window(int qh, int kh, int bq) {
-  if (bq < 0) return {1, 0};
-  if (qh == HALF_NOISY) return kh == HALF_NOISY ? BlockWindow{bq, bq} : BlockWindow{0, bq - 1};
-  return kh == HALF_CLEAN ? BlockWindow{0, bq} : BlockWindow{1, 0};
-}
-// The same rule seen from one key (block bk): window of visible query blocks.
-__device__ inline BlockWindow query_window(int qh, int kh, int bk) {
-  if (qh == HALF_NOISY) return kh == HALF_NOISY ? BlockWindow{bk, bk} : BlockWindow{bk + 1, 0x7fffffff};
-  return kh == HALF_CLEAN ? BlockWindow{bk, 0x7fffffff} : BlockWindow{1, 0};
-}
 __device__ inline void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ inline bf16x8 lds_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+// 8 consecutive elements (one 16-byte chunk) of a swizzled tile; col % 8 == 0.
+template <int D>
+__device__ inline bf16x8 lds_row8(const bf16* tile, int row, int col) {
+  return lds_bf16x8(tile + tile_idx<D>(row, col));
+}
 
 // Eight consecutive accumulator values as a bf16 MFMA operand (round to nearest even).
 __device__ inline bf16x8 pack8(const f32x16& acc, int base) {

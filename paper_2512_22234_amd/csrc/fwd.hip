@@ -7,13 +7,15 @@
 // exchange (lane l <-> l+32) per key tile and the running row sum stays a
 // per-lane partial until the epilogue.  O^T = V^T P^T reuses the score
 // accumulator directly as the bf16 B operand; its A operand V^T is read from
-// the row-major V tile with the transposing LDS read (see device.hpp).
+// the V tile with the transposing LDS read (see device.hpp).
 //
 // Key tiles (64 keys) are visited in the order given by the exact tile
 // classification: FULL tiles run with no per-element test, PARTIAL tiles
-// apply the visibility rule per element, EMPTY tiles are never loaded.  K and
-// V tiles are double-buffered in LDS; the next tile's global loads are in
-// flight while the current one is computed.
+// apply the visibility window per element, EMPTY tiles are never loaded.  K
+// and V tiles are copied into LDS asynchronously (global_load_lds) one tile
+// ahead, double-buffered, so the copy runs under the current tile's compute.
+// The online softmax keeps a reference maximum per row that only moves when
+// the scores exceed it by a margin, so the O rescale is rare.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -33,20 +35,24 @@ struct FwdParams {
 template <int D>
 struct FwdSmem {
   static constexpr int BN = FWD_BN;
-  static constexpr int KS = D + 8;  // K/V row stride (elements), 16-byte pad against bank conflicts
-  bf16 k[2][BN * KS];
-  bf16 v[2][BN * KS];
-  alignas(16) int kblk[2][BN];
+  static constexpr uint32_t TILE = BN * D * 2;  // bytes per swizzled tile
+  bf16 k[2][BN * D];  // byte offset buf * TILE
+  bf16 v[2][BN * D];  // byte offset (2 + buf) * TILE
 };
+
+// The reference maximum of a row moves only when the row's scores exceed it
+// by more than this (log2 units), so the accumulator rescale is rare; P stays
+// below 2^8 and the final O / l and LSE are unchanged (both use the same
+// reference).
+constexpr float RESCALE_SLACK = 8.0f;
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   constexpr int BM = FWD_BM, BN = FWD_BN;
   constexpr int DS = D / 16, DB = D / 32, KB = BN / 32, PC = BN / 16;
-  constexpr int KS = FwdSmem<D>::KS;
-  constexpr int NCH = BN * D / 8 / 256;  // 16-byte chunks per thread, for each of K and V
-  static_assert(NCH * 256 * 8 == BN * D, "tile must split evenly over 256 threads");
+  constexpr uint32_t TILE = FwdSmem<D>::TILE;
   __shared__ FwdSmem<D> sm;
+  char* lds = reinterpret_cast<char*>(&sm);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
@@ -61,13 +67,26 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
+  const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;  // first rows of the tile's first and last block
 
   const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
 
   const int r = q0 + w * 32 + l32;  // this lane's query row (local to its half)
   const bool qvalid = r < q1;
-  const int bq = qvalid ? r / S : QBLK_INVALID;
+  const int qblock0 = qvalid ? (r / S) * S : 0;
   const int prow = qh * L + r;
+
+  const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
+  const int T = kl.count();
+  const TileCopy<D, BN, 256> copy(tid);
+  auto issue = [&](int t) {
+    int kh, j;
+    kl.at(t, kh, j);
+    const size_t hb = kvbase + (size_t)kh * L * D;
+    copy.issue(p.K + hb, j * BN, L, lds, (t & 1) * TILE, tid);
+    copy.issue(p.V + hb, j * BN, L, lds, (2 + (t & 1)) * TILE, tid);
+  };
+  if (T > 0) issue(0);
 
   bf16x8 qreg[DS];
   {
@@ -76,61 +95,26 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
     for (int s = 0; s < DS; ++s)
       qreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(qp + 16 * s) : zero_bf16x8();
   }
-
-  const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
-  const int T = kl.count();
-
-  u32x4 kst[NCH], vst[NCH];
-  int kbst = 0;
-  auto load_tile = [&](int t) {
-    int kh, j;
-    kl.at(t, kh, j);
-    const bf16* kp = p.K + kvbase + (size_t)kh * L * D;
-    const bf16* vp = p.V + kvbase + (size_t)kh * L * D;
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      kst[u] = ld16_rows(kp, j * BN + row, L, D, col8 * 8);
-      vst[u] = ld16_rows(vp, j * BN + row, L, D, col8 * 8);
-    }
-    if (tid < BN) {
-      const int key = j * BN + tid;
-      kbst = key < L ? key / S : KBLK_INVALID;
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = tid + 256 * u;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      st16(&sm.k[buf][row * KS + col8 * 8], kst[u]);
-      st16(&sm.v[buf][row * KS + col8 * 8], vst[u]);
-    }
-    if (tid < BN) sm.kblk[buf][tid] = kbst;
-  };
+  const LdsOperands<D> ops(lane);
 
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[db][e] = 0.f;
-  float m = -INFINITY, lsum = 0.f;
+  float m = -INFINITY, lsum = 0.f;  // reference max (log2 units) and row sum relative to it
 
-  if (T > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  wait_global_loads();  // Q rows are in registers; the loop only waits on its own prefetch
+  wait_global_loads();
   __syncthreads();
 
   for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < T) load_tile(t + 1);
+    const uint32_t kbase = (t & 1) * TILE + ops.row_rel;
+    const uint32_t vb0 = (2 + (t & 1)) * TILE + ops.tr_rel0, vb1 = (2 + (t & 1)) * TILE + ops.tr_rel1;
+    if (t + 1 < T) issue(t + 1);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
-    const int cls = classify_pair(qh, q0, q1, kh, k0, k1, S, (q1 - q0) == BM && (k1 - k0) == BN);
+    const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
     if (cls != TILE_EMPTY) {
       f32x16 sacc[KB];
 #pragma unroll
@@ -141,47 +125,51 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int s = 0; s < DS; ++s)
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const bf16x8 a = lds_bf16x8(&sm.k[buf][(kb * 32 + l32) * KS + 16 * s + 8 * g2]);
-          sacc[kb] = mfma32(a, qreg[s], sacc[kb]);
-        }
+        for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(lds, kbase, s, kb), qreg[s], sacc[kb]);
       if (cls == TILE_PARTIAL) {
-        const BlockWindow win = key_window(qh, kh, bq);
+        // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
+        const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
+        const unsigned span = (unsigned)(win.hi - win.lo);
+        const int rel = k0 + 4 * g2 - win.lo;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int4 kb4 = *reinterpret_cast<const int4*>(&sm.kblk[buf][kb * 32 + 8 * i + 4 * g2]);
-            const int kbv[4] = {kb4.x, kb4.y, kb4.z, kb4.w};
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj)
-              sacc[kb][4 * i + jj] = win.has(kbv[jj]) ? sacc[kb][4 * i + jj] : -INFINITY;
-          }
+            for (int jj = 0; jj < 4; ++jj) {
+              const unsigned pos = (unsigned)(rel + kb * 32 + 8 * i + jj);
+              sacc[kb][4 * i + jj] = pos < span ? sacc[kb][4 * i + jj] : -INFINITY;
+            }
       }
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m, mx * p.c);
-      const float muse = (mnew == -INFINITY) ? 0.f : mnew;
-      const float alpha = fast_exp2(m - muse);
-      m = mnew;
-      float ps = 0.f;
+        for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[kb][e], sacc[kb][e + 1]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.c;
+      // move the reference only when this tile's max is far above it
+      const bool grow = mx > m + RESCALE_SLACK;
+      if (__any(grow)) {
+        // lanes that do not grow keep factor 1 (their m may still be -inf);
+        // a growing lane whose m is -inf gets exp2(-inf) = 0
+        const float alpha = grow ? fast_exp2(m - mx) : 1.f;
+        const float mnew = grow ? mx : m;
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
+        m = mnew;
+      }
+      const float muse = (m == -INFINITY) ? 0.f : m;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float x = fast_exp2(sacc[kb][e] * p.c - muse);
           sacc[kb][e] = x;
-          ps += x;
+          lsum += x;
         }
-      lsum = lsum * alpha + ps;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
       bf16x8 pb[PC];
 #pragma unroll
       for (int c = 0; c < PC; ++c) pb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
@@ -189,14 +177,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int c = 0; c < PC; ++c)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16x8 a = lds_read_tr(sm.v[buf], KS, 16 * c, db * 32, lane);
-          oacc[db] = mfma32(a, pb[c], oacc[db]);
-        }
+        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(lds, vb0, vb1, c, db), pb[c], oacc[db]);
     }
     compute_fence();
-    if (t + 1 < T) store_tile(buf ^ 1);
-    __syncthreads();
+    wait_global_loads();  // this wave's part of the next tile has landed in LDS
+    __syncthreads();      // ... for every wave, and every wave is done with this buffer
   }
 
   const float lt = lsum + __shfl_xor(lsum, 32);

@@ -64,6 +64,67 @@ BD_HD int classify_pair(int qh, int q0, int q1, int kh, int k0, int k1, int S, b
   return cls;
 }
 
+// Division-free forms of classify_pair used inside the kernels.  For a fixed
+// tile whose block range is [lo, hi], pass A = lo*S and B = hi*S (the first
+// positions of its first and last block); the moving tile is [m0, m1).  The
+// comparisons are those of classify_pair with both sides multiplied by S.
+//
+// Fixed query tile (half qh), moving key tile (half kh).
+BD_HD int classify_vs_query_tile(int qh, int A, int B, int S, int kh, int k0, int k1, bool full_size) {
+  int cls;
+  if (qh == HALF_NOISY && kh == HALF_NOISY) {
+    if (k0 >= B + S || k1 <= A) return TILE_EMPTY;
+    cls = (A == B && k0 >= A && k1 <= A + S) ? TILE_FULL : TILE_PARTIAL;
+  } else if (qh == HALF_NOISY) {
+    if (k0 >= B) return TILE_EMPTY;
+    cls = (k1 <= A) ? TILE_FULL : TILE_PARTIAL;
+  } else if (kh == HALF_CLEAN) {
+    if (k0 >= B + S) return TILE_EMPTY;
+    cls = (k1 <= A + S) ? TILE_FULL : TILE_PARTIAL;
+  } else {
+    return TILE_EMPTY;
+  }
+  if (cls == TILE_FULL && !full_size) cls = TILE_PARTIAL;
+  return cls;
+}
+// Fixed key tile (half kh), moving query tile (half qh).
+BD_HD int classify_vs_key_tile(int kh, int A, int B, int S, int qh, int q0, int q1, bool full_size) {
+  int cls;
+  if (qh == HALF_NOISY && kh == HALF_NOISY) {
+    if (q1 <= A || q0 >= B + S) return TILE_EMPTY;
+    cls = (A == B && q0 >= A && q1 <= A + S) ? TILE_FULL : TILE_PARTIAL;
+  } else if (qh == HALF_NOISY) {
+    if (q1 <= A + S) return TILE_EMPTY;
+    cls = (q0 >= B + S) ? TILE_FULL : TILE_PARTIAL;
+  } else if (kh == HALF_CLEAN) {
+    if (q1 <= A) return TILE_EMPTY;
+    cls = (q0 >= B) ? TILE_FULL : TILE_PARTIAL;
+  } else {
+    return TILE_EMPTY;
+  }
+  if (cls == TILE_FULL && !full_size) cls = TILE_PARTIAL;
+  return cls;
+}
+
+// Visible positions of the other half for one row, as a half-open window of
+// local positions [lo, hi) (empty when lo == hi).  pos_block_start = b*S for
+// the row's block b.  Past-the-end rows pass valid = false.
+struct PosWindow {
+  int lo, hi;
+};
+// For a query (block start a = bq*S) looking at keys of half kh.
+BD_HD PosWindow keys_visible_from(int qh, int kh, int a, int L, int S, bool valid) {
+  if (!valid) return {0, 0};
+  if (qh == HALF_NOISY) return kh == HALF_NOISY ? PosWindow{a, imin(L, a + S)} : PosWindow{0, a};
+  return kh == HALF_CLEAN ? PosWindow{0, imin(L, a + S)} : PosWindow{0, 0};
+}
+// For a key (block start a = bk*S) seen by queries of half qh.
+BD_HD PosWindow queries_seeing(int kh, int qh, int a, int L, int S, bool valid) {
+  if (!valid) return {0, 0};
+  if (qh == HALF_NOISY) return kh == HALF_NOISY ? PosWindow{a, imin(L, a + S)} : PosWindow{imin(L, a + S), L};
+  return kh == HALF_CLEAN ? PosWindow{a, L} : PosWindow{0, 0};
+}
+
 // Key tiles visited by query tile (qh, i): clean key tiles [0, nclean) then,
 // for a noisy query tile, noisy key tiles [noisy0, noisy0 + nnoisy).
 struct KeyTileList {

@@ -81,6 +81,14 @@ def test_tile_walks_visit_each_nonempty_pair_once(L, S, BM, BN):
         np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"by_key={by_key}")
 
 
+@pytest.mark.parametrize("by_key", [False, True])
+def test_kernel_mask_windows_match_oracle_mask(by_key):
+    for L in (1, 2, 3, 5, 8, 13, 16, 31, 64):
+        for S in range(1, L + 2):
+            got = bd.bd_attn_mask_windows_host(L, S, by_key).astype(bool)
+            np.testing.assert_array_equal(got, oracle.visibility_mask(L, S), err_msg=f"L={L} S={S}")
+
+
 def test_classifier_tile_counts_8b_shape():
     # L=2048, S=4 with 128x128 tiles: per (b, h) 1024 pairs; 240 FULL, 48 PARTIAL, 736 EMPTY
     c = bd.bd_attn_classify_tiles_host(2048, 4, 128, 128)
