@@ -47,6 +47,54 @@ def log(msg: str):
     print(msg, file=sys.stderr, flush=True)
 
 
+HERE = os.path.dirname(os.path.abspath(__file__))
+COUNTERS_FILE = os.path.join(HERE, "profiles", "bd_attn_8b_hbm_traffic.md")
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the library's kernel sources (file names and contents)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(HERE, "paper_2512_22234_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when there is none for this workload or the kernel sources changed
+    since the counters were taken (the summary records the source hash)."""
+    try:
+        text = open(COUNTERS_FILE).read()
+    except OSError:
+        return None
+    start = text.find("```json")
+    if start < 0:
+        return None
+    rec = json.loads(text[start + 7:text.index("```", start + 7)])
+    if rec.get("source_sha256") != kernel_source_hash() or rec.get("workload") != workload:
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else int(k["hbm_bytes_per_launch"])
+
+
+def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
+    """A plain device-to-device copy of known size, the reference the HBM
+    byte counters are scaled by (run under rocprofv3 --pmc)."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[copy] {reps} copies of {nbytes} bytes (each reads {nbytes} and writes {nbytes} bytes)")
+
+
 def cpu_baseline(w, budget_s: float, max_groups: int):
     import numpy as np
     import oracle
@@ -93,6 +141,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
     ap.add_argument("--cpu-max-groups", type=int, default=4)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the plain 256 MiB copy used to scale the HBM byte counters")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -100,6 +150,10 @@ def main():
         print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
               "the block-diffusion attention path here has no multi-GPU mode.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import torch
     import paper_2512_22234_amd as bd
@@ -203,7 +257,9 @@ def main():
                    "visible_pairs_per_head": visible_pairs(L, S),
                    "flops_per_step": f_fwd + f_bwd, "fwd_ms": round(t_fwd, 5), "bwd_ms": round(t_bwd, 5)},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(dom, w.name), "traffic_unit": "HBM bytes per launch",
+                     "algorithmic_flops_per_launch": alg[dom]},
         "kernels": kernels,
         "cpu_baseline": cpu,
     }
