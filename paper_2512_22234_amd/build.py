@@ -30,9 +30,23 @@ CFLAGS = [
 ]
 
 
+# Per-file additions.  The forward kernel: no NaN semantics (its inputs are
+# finite or -inf, so fmax needs no quieting of its operands), and MFMAs in
+# their VGPR form (the scores are consumed by VALU code, so AGPR accumulators
+# would be copied back every tile).
+FILE_FLAGS = {
+    "fwd.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
+def compile_flags(src: str) -> list:
+    """hipcc flags (without -c / -o) that build.py uses for csrc/<src>."""
+    return [*CFLAGS, *FILE_FLAGS.get(src, [])]
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *compile_flags(src), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
@@ -48,6 +62,12 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    # every kernel launched from host code must have its launch stub defined
+    r = subprocess.run(["nm", "-u", tmp], capture_output=True, text=True)
+    missing = [l.split()[-1] for l in r.stdout.splitlines() if "__device_stub__" in l]
+    if missing:
+        os.remove(tmp)
+        raise RuntimeError(f"kernel launch stubs missing from the host objects: {missing}")
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

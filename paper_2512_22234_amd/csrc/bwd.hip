@@ -78,10 +78,11 @@ template <int D>
 struct DkvSmem {
   static constexpr int BM = DKV_BM;
   static constexpr uint32_t TILE = BM * D * 2;  // bytes per swizzled tile
-  bf16 q[2][BM * D];   // byte offset buf * TILE
-  bf16 dO[2][BM * D];  // byte offset (2 + buf) * TILE
-  alignas(16) float lse2[2][BM];
-  alignas(16) float dlt[2][BM];
+  // one contiguous region per buffer: Q tile, dO tile, lse2 and delta rows
+  static constexpr uint32_t DO_OFF = TILE, LSE_OFF = 2 * TILE, DLT_OFF = 2 * TILE + 4 * BM;
+  static constexpr uint32_t BUF = 2 * TILE + 8 * BM;  // a multiple of 256 bytes
+  static_assert(BUF % 256 == 0, "operand addressing needs 256-byte aligned tiles");
+  alignas(256) char buf[2][BUF];
 };
 
 // dK/dV accumulation.  PIN keeps the accumulators in AGPRs through inline-asm
@@ -99,13 +100,9 @@ __device__ inline f32x16 acc_zero() {
   return z;
 }
 template <bool PIN>
-__device__ inline void acc_mfma(f32x16& acc, const bf16x8& a, const bf16x8& b, bool fresh) {
-  if constexpr (PIN) {
-    if (fresh) mfma32_agpr<true>(acc, a, b);
-    else mfma32_agpr<false>(acc, a, b);
-  } else {
-    acc = mfma32(a, b, acc);
-  }
+__device__ inline void acc_mfma(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  if constexpr (PIN) mfma32_agpr(acc, a, b);
+  else acc = mfma32(a, b, acc);
 }
 
 // Position in a head-major walk over (query head g, query tile u).
@@ -124,9 +121,8 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   constexpr int BM = DKV_BM, BN = DKV_BN;
   constexpr int DS = D / 16, DB = D / 32, QB = BM / 32;
   constexpr bool PIN = D == 128;
-  constexpr uint32_t TILE = DkvSmem<D>::TILE;
-  __shared__ DkvSmem<D> sm;
-  char* lds = reinterpret_cast<char*>(&sm);
+  using Smem = DkvSmem<D>;
+  __shared__ Smem sm;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
@@ -159,20 +155,20 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int T = t1 - t0;
 
   const TileCopy<D, BM, 256> copy(tid);
-  auto issue = [&](WalkPos wp, int buf) {
+  auto issue = [&](WalkPos wp, char* dst) {
     int qh, i;
     ql.at(wp.u, qh, i);
     const size_t row0 = ((size_t)b * p.Hq + hk * p.G + wp.g) * N + qh * L;  // first row of the half
-    copy.issue(p.Q + row0 * D, i * BM, L, lds, buf * TILE, tid);
-    copy.issue(p.dO + row0 * D, i * BM, L, lds, (2 + buf) * TILE, tid);
-    if (w == 0) async_load_row_floats(p.lse2 + row0, i * BM, L, sm.lse2[buf], lane);
-    if (w == 1) async_load_row_floats(p.delta + row0, i * BM, L, sm.dlt[buf], lane);
+    copy.issue(p.Q + row0 * D, i * BM, L, dst, 0);
+    copy.issue(p.dO + row0 * D, i * BM, L, dst, Smem::DO_OFF);
+    if (w == 0) async_load_row_floats(p.lse2 + row0, i * BM, L, reinterpret_cast<float*>(dst + Smem::LSE_OFF), lane);
+    if (w == 1) async_load_row_floats(p.delta + row0, i * BM, L, reinterpret_cast<float*>(dst + Smem::DLT_OFF), lane);
   };
   WalkPos cur = {0, 0};
   if (per_g > 0) cur = {t0 / per_g, t0 % per_g};
   WalkPos nxt = cur;
   if (T > 0) {
-    issue(cur, 0);
+    issue(cur, sm.buf[0]);
     nxt.next(per_g);
   }
 
@@ -194,13 +190,15 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   wait_global_loads();
   __syncthreads();
 
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    const uint32_t qrb = buf * TILE + ops.row_rel, drb = (2 + buf) * TILE + ops.row_rel;
-    const uint32_t qt0 = buf * TILE + ops.tr_rel0, qt1 = buf * TILE + ops.tr_rel1;
-    const uint32_t dt0 = (2 + buf) * TILE + ops.tr_rel0, dt1 = (2 + buf) * TILE + ops.tr_rel1;
+  // One query tile.  The current buffer and the one the next tile is copied
+  // into are distinct restrict-qualified pointers: the alias scopes this gives
+  // every LDS access let the compiler see that the copy in flight cannot
+  // overwrite the tile being read, so it does not wait for the copy before
+  // the reads (the wait at the end of the step covers it).
+  auto tile_step = [&](const char* __restrict__ bc, char* __restrict__ bn, int t) __attribute__((always_inline)) {
+    const char* bd = bc + Smem::DO_OFF;
     if (t + 1 < T) {
-      issue(nxt, buf ^ 1);
+      issue(nxt, bn);
       nxt.next(per_g);
     }
     int qh, i;
@@ -225,14 +223,14 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
         // S[q][key] = sum_d Q[q][d] K[key][d];  dP[q][key] = sum_d dO[q][d] V[key][d]
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
-          sacc = mfma32(lds_rows<D>(lds, qrb, s, qb), kreg[s], sacc);
-          dpacc = mfma32(lds_rows<D>(lds, drb, s, qb), vreg[s], dpacc);
+          sacc = mfma32(lds_rows<D>(bc, ops.row_rel, s, qb), kreg[s], sacc);
+          dpacc = mfma32(lds_rows<D>(bd, ops.row_rel, s, qb), vreg[s], dpacc);
         }
 #pragma unroll
         for (int i4 = 0; i4 < 4; ++i4) {
           const int rr = qb * 32 + 8 * i4 + 4 * g2;
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sm.lse2[buf][rr]);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sm.dlt[buf][rr]);
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(bc + Smem::LSE_OFF + 4 * rr);
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(bc + Smem::DLT_OFF + 4 * rr);
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             float pv = fast_exp2(sacc[4 * i4 + jj] * p.c - l4[jj]);
@@ -248,12 +246,15 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
           const int c = 2 * qb + h;
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            acc_mfma<PIN>(dvacc[db], lds_tr<D>(lds, dt0, dt1, c, db), pb, db == 0);
-            acc_mfma<PIN>(dkacc[db], lds_tr<D>(lds, qt0, qt1, c, db), dsb, db == 0);
+            acc_mfma<PIN>(dvacc[db], lds_tr<D>(bd, ops.tr_rel0, ops.tr_rel1, c, db), pb);
+            acc_mfma<PIN>(dkacc[db], lds_tr<D>(bc, ops.tr_rel0, ops.tr_rel1, c, db), dsb);
           }
         }
       }
     }
+  };
+  for (int t = 0; t < T; ++t) {
+    tile_step(sm.buf[t & 1], sm.buf[(t + 1) & 1], t);
     compute_fence();
     wait_global_loads();
     __syncthreads();
@@ -367,14 +368,14 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
-  auto issue = [&](int t) {
+  auto issue = [&](int t, char* kdst, char* vdst) {
     int kh, j;
     kl.at(t, kh, j);
     const size_t hb = kvbase + (size_t)kh * L * D;
-    copy.issue(p.K + hb, j * BN, L, lds, (t & 1) * TILE, tid);
-    copy.issue(p.V + hb, j * BN, L, lds, (2 + (t & 1)) * TILE, tid);
+    copy.issue(p.K + hb, j * BN, L, kdst, 0);
+    copy.issue(p.V + hb, j * BN, L, vdst, 0);
   };
-  if (T > 0) issue(0);
+  if (T > 0) issue(0, lds, lds + 2 * TILE);
 
   bf16x8 qreg[DS], doreg[DS];
 #pragma unroll
@@ -395,11 +396,12 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   wait_global_loads();
   __syncthreads();
 
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    const uint32_t krb = buf * TILE + ops.row_rel, vrb = (2 + buf) * TILE + ops.row_rel;
-    const uint32_t kt0 = buf * TILE + ops.tr_rel0, kt1 = buf * TILE + ops.tr_rel1;
-    if (t + 1 < T) issue(t + 1);
+  // One key tile; restrict-qualified current and next buffers as in the
+  // forward kernel, so the copy in flight does not make the compiler wait
+  // before the reads of the current tile.
+  auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
+                       char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
+    if (t + 1 < T) issue(t + 1, knxt, vnxt);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
@@ -418,8 +420,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       for (int s = 0; s < DS; ++s)
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
-          sacc[kb] = mfma32(lds_rows<D>(lds, krb, s, kb), qreg[s], sacc[kb]);
-          dpacc[kb] = mfma32(lds_rows<D>(lds, vrb, s, kb), doreg[s], dpacc[kb]);
+          sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
+          dpacc[kb] = mfma32(lds_rows<D>(vcur, ops.row_rel, s, kb), doreg[s], dpacc[kb]);
         }
       const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
       const unsigned span = cls == TILE_PARTIAL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
@@ -442,8 +444,13 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 #pragma unroll
       for (int c = 0; c < PC; ++c)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(lds, kt0, kt1, c, db), dsb[c], dqacc[db]);
+        for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(kcur, ops.tr_rel0, ops.tr_rel1, c, db), dsb[c], dqacc[db]);
     }
+  };
+  for (int t = 0; t < T; ++t) {
+    char* cur = lds + (t & 1) * TILE;
+    char* nxt = lds + ((t + 1) & 1) * TILE;
+    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
     compute_fence();
     wait_global_loads();
     __syncthreads();

@@ -43,18 +43,18 @@ __device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& 
 // the register allocator from parking them in AGPRs between iterations and
 // copying them through VGPRs on every pass.  The compiler's hazard tracking
 // does not see inside the asm, so the two waits it would insert are explicit:
-//  - a VALU result feeding the MFMA as A or B needs two wait states; FRESH
-//    adds them (use it for the first MFMA after the operands are computed);
+//  - a VALU result feeding the MFMA as A or B needs two wait states; every
+//    call starts with them (s_nop 2 gives three), since the compiler may
+//    schedule the producing VALU instruction right before any of these MFMAs;
 //  - results must not be read by other instructions until mfma_drain() has
 //    run on every accumulator (it ties them as operands, so no read can be
 //    scheduled above it).
 // Back-to-back accumulation into the same registers needs no wait states.
-template <bool FRESH = false>
+// The asm is not volatile: its operands carry every dependency, and a volatile
+// statement would pin the LDS reads that feed it in place (no read could be
+// hoisted above an earlier MFMA), exposing the full LDS latency on every MFMA.
 __device__ inline void mfma32_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  if constexpr (FRESH)
-    asm volatile("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-  else
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  asm("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 // A zero accumulator defined directly in AGPRs (an MFMA of zero operands), so
 // that every definition and loop use of an mfma32_agpr accumulator is AGPR.
@@ -168,39 +168,57 @@ __device__ inline bf16x8 lds_tr(const char* lds, uint32_t b0, uint32_t b1, int c
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Per-lane element offsets of the chunks a lane copies in async_load_tile
-// (they do not depend on which tile is copied).
+// Asynchronous copy of a tile of NR rows x D bf16 from a row-major global
+// array into a swizzled LDS tile with global_load_lds (16 bytes per lane, the
+// LDS address of lane i is M0 + 16*i).  Each wave instruction fills 1 KiB of
+// the tile contiguously; lane i fetches the global chunk that belongs at LDS
+// chunk p (the XOR swizzle is its own inverse).  The per-lane byte offsets of
+// those chunks do not depend on which tile is copied, so they are computed
+// once; a whole tile then costs one scalar base per instruction.  Rows past
+// nrows are clamped to the last row: the kernels mask them out, so they only
+// need finite data.  Completion is tracked by the wave's vmcnt
+// (wait_global_loads) and must be followed by a workgroup barrier before
+// other waves read the tile.
 template <int D, int NR, int NT>
 struct TileCopy {
   static constexpr int CPR = D / 8;
   static constexpr int NW = NT / 64;
   static constexpr int NI = NR * CPR / NT;
   static_assert(NI * NT == NR * CPR, "tile must split evenly over the workgroup");
-  int goff[NI];  // element offset of the source chunk relative to the tile's first row
+  // (The source addresses are passed to the builtin as const void*: with a
+  // const char* argument the host compilation pass silently dropped the launch
+  // stub of one kernel using this copy.)
+  uint32_t boff[NI];  // byte offset of the source chunk from the tile's first row
+  int wave;           // wave index, uniform
   __device__ explicit TileCopy(int tid) {
-    const int w = tid >> 6, lane = tid & 63;
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
-      const int p = (u * NW + w) * 64 + lane;
+      const int p = (u * NW + wave) * 64 + lane;
       const int row = p / CPR;
-      goff[u] = row * D + (((p % CPR) ^ chunk_swizzle<D>(row)) << 3);
+      boff[u] = (uint32_t)(2 * (row * D + (((p % CPR) ^ chunk_swizzle<D>(row)) << 3)));
     }
   }
   // Copy rows [row0, row0 + NR) of src (clamped to < nrows) into the tile at
   // LDS byte offset tile_off of lds (a multiple of 1 KiB).
-  __device__ void issue(const bf16* src, int row0, int nrows, char* lds, uint32_t tile_off, int tid) const {
-    const int w = tid >> 6;
-    const bool whole = row0 + NR <= nrows;
+  __device__ void issue(const bf16* src, int row0, int nrows, char* lds, uint32_t tile_off) const {
+    const char* base = reinterpret_cast<const char*>(src + (size_t)row0 * D);
+    if (row0 + NR <= nrows) {
 #pragma unroll
-    for (int u = 0; u < NI; ++u) {
-      int off = row0 * D + goff[u];
-      if (!whole) {
-        const int row = goff[u] / D;
-        off = imin(row0 + row, nrows - 1) * D + (goff[u] - row * D);
+      for (int u = 0; u < NI; ++u)
+        __builtin_amdgcn_global_load_lds((const void*)(base + boff[u]),
+                                         (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + wave) * 1024),
+                                         16, 0, 0);
+    } else {
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        const int row = (int)(boff[u] / (2 * D));
+        const int over = imax(0, row0 + row - (nrows - 1));  // rows to step back
+        __builtin_amdgcn_global_load_lds((const void*)(base + boff[u] - (size_t)over * 2 * D),
+                                         (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + wave) * 1024),
+                                         16, 0, 0);
       }
-      __builtin_amdgcn_global_load_lds(src + off,
-                                       (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + w) * 1024),
-                                       16, 0, 0);
     }
   }
 };

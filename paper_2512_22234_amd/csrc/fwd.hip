@@ -46,6 +46,17 @@ struct FwdSmem {
 // reference).
 constexpr float RESCALE_SLACK = 8.0f;
 
+// Combine a per-lane value over the two half-waves (lanes l and l + 32 hold
+// the two halves of one query row's keys) with v_permlane32_swap.
+__device__ inline float halves_max(float x) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+__device__ inline float halves_sum(float x) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+}
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   constexpr int BM = FWD_BM, BN = FWD_BN;
@@ -79,14 +90,15 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
-  auto issue = [&](int t) {
+  auto issue = [&](int t, char* kdst, char* vdst) {
     int kh, j;
     kl.at(t, kh, j);
     const size_t hb = kvbase + (size_t)kh * L * D;
-    copy.issue(p.K + hb, j * BN, L, lds, (t & 1) * TILE, tid);
-    copy.issue(p.V + hb, j * BN, L, lds, (2 + (t & 1)) * TILE, tid);
+    copy.issue(p.K + hb, j * BN, L, kdst, 0);
+    copy.issue(p.V + hb, j * BN, L, vdst, 0);
   };
-  if (T > 0) issue(0);
+
+  if (T > 0) issue(0, lds, lds + 2 * TILE);
 
   bf16x8 qreg[DS];
   {
@@ -107,10 +119,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   wait_global_loads();
   __syncthreads();
 
-  for (int t = 0; t < T; ++t) {
-    const uint32_t kbase = (t & 1) * TILE + ops.row_rel;
-    const uint32_t vb0 = (2 + (t & 1)) * TILE + ops.tr_rel0, vb1 = (2 + (t & 1)) * TILE + ops.tr_rel1;
-    if (t + 1 < T) issue(t + 1);
+  // One key tile.  The current K/V tiles and the buffers the next tile is
+  // copied into are distinct restrict-qualified pointers: the alias scopes
+  // this gives every LDS access let the compiler see that the copy in flight
+  // cannot overwrite the tiles being read, so it does not wait for the copy
+  // before the reads (the wait at the end of the step covers it).
+  auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
+                       char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
+    if (t + 1 < T) issue(t + 1, knxt, vnxt);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
@@ -125,7 +141,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int s = 0; s < DS; ++s)
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(lds, kbase, s, kb), qreg[s], sacc[kb]);
+        for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
       if (cls == TILE_PARTIAL) {
         // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
         const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
@@ -146,10 +162,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[kb][e], sacc[kb][e + 1]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.c;
+      mx = halves_max(mx) * p.c;
       // move the reference only when this tile's max is far above it
       const bool grow = mx > m + RESCALE_SLACK;
       if (__any(grow)) {
+        asm volatile("" ::: "memory");  // rare: keep the rescale out of the common path
         // lanes that do not grow keep factor 1 (their m may still be -inf);
         // a growing lane whose m is -inf gets exp2(-inf) = 0
         const float alpha = grow ? fast_exp2(m - mx) : 1.f;
@@ -177,14 +194,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int c = 0; c < PC; ++c)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(lds, vb0, vb1, c, db), pb[c], oacc[db]);
+        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, c, db), pb[c], oacc[db]);
     }
+  };
+  for (int t = 0; t < T; ++t) {
+    char* cur = lds + (t & 1) * TILE;
+    char* nxt = lds + ((t + 1) & 1) * TILE;
+    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
     compute_fence();
     wait_global_loads();  // this wave's part of the next tile has landed in LDS
     __syncthreads();      // ... for every wave, and every wave is done with this buffer
   }
 
-  const float lt = lsum + __shfl_xor(lsum, 32);
+  const float lt = halves_sum(lsum);
   if (qvalid) {
     const float inv = 1.f / lt;
     bf16* op = p.O + ((size_t)bh * N + prow) * D + 4 * g2;

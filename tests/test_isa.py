@@ -49,13 +49,13 @@ def _kernel_instructions(asm: str, name: str):
         if s.startswith(";;#ASMEND"):
             in_asm = False
             continue
+        if s.startswith(".Lfunc_end"):
+            break
         s = s.split(";")[0].strip()
         if not s or s.startswith(".") or s.endswith(":"):
             continue
         parts = s.replace(",", " ").split()
         out.append((parts[0], parts[1:], in_asm))
-        if parts[0] == "s_endpgm":
-            break
     return out
 
 
@@ -91,10 +91,10 @@ def _hazards(insts):
 def dkdv_asm(tmp_path_factory):
     if not Path(HIPCC).exists():
         pytest.skip("hipcc not available")
+    from paper_2512_22234_amd.build import compile_flags
     out = tmp_path_factory.mktemp("isa") / "bwd.s"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang",
-           "-packed-fp32-ops", f"-I{ROOT / 'include'}", f"-I{CSRC}", "--cuda-device-only", "-S", "-o", str(out),
-           str(CSRC / "bwd.hip")]
+    flags = [f for f in compile_flags("bwd.hip") if f != "-fPIC"]
+    cmd = [HIPCC, *flags, f"-I{CSRC}", "--cuda-device-only", "-S", "-o", str(out), str(CSRC / "bwd.hip")]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stderr[-2000:]
     return out.read_text()
@@ -118,6 +118,7 @@ def test_checker_flags_early_read():
         ";;#ASMSTART", "s_nop 7", ";;#ASMEND",
         "v_accvgpr_read_b32 v21, a4",
         "s_endpgm",
+        ".Lfunc_end0:",
     ])
     problems, _ = _hazards(_kernel_instructions(asm, "k"))
     assert any("before the drain" in p for p in problems)
