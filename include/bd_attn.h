@@ -23,8 +23,9 @@
  *   BD_ATTN_BF16 (0): bfloat16 — the compute path;
  *   BD_ATTN_FP32 (1): float32, rounded to bfloat16 inside the library (the
  *                     arithmetic is the bf16 path) and written back as float32.
- * D must be 64 or 128.  S >= L behaves as S = L.  S need not divide L (the
- * last block is then shorter).  scale <= 0 selects 1/sqrt(D).
+ * D must be 64 or 128; 1 <= L <= 2^22.  S >= L behaves as S = L.  S need
+ * not divide L (the last block is then shorter).  scale <= 0 selects
+ * 1/sqrt(D).
  *
  * Ownership and ordering: the caller allocates every buffer, including the
  * workspace (size from bd_attn_workspace_bytes, at least 16-byte aligned).  The
@@ -53,7 +54,7 @@ extern "C" {
 
 enum bd_attn_status {
   BD_ATTN_OK = 0,
-  BD_ATTN_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, B,L,S<1, Hq%Hkv!=0, overlap */
+  BD_ATTN_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, B,L,S<1, L>2^22, Hq%Hkv!=0, overlap */
   BD_ATTN_ERR_UNSUPPORTED = 2,      /* D not in {64,128}, unknown dtype */
   BD_ATTN_ERR_WORKSPACE_TOO_SMALL = 3, /* checked before overlap with the workspace */
   BD_ATTN_ERR_HIP = 4               /* a HIP launch reported an error */

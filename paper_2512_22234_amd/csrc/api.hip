@@ -21,7 +21,9 @@ struct Layout {
 };
 
 bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
-  return B >= 1 && L >= 1 && S >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 && L <= (1 << 28);
+  // L <= 2^22: the kernels address one head's 2L rows of D <= 128 bf16 values
+  // through 32-bit buffer offsets (2L * D * 2 bytes < 2^31)
+  return B >= 1 && L >= 1 && S >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 && L <= (1 << 22);
 }
 
 Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {

@@ -155,14 +155,19 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int T = t1 - t0;
 
   const TileCopy<D, BM, 256> copy(tid);
+  // Q, dO, lse2 and delta of one query head (2L rows each)
   auto issue = [&](WalkPos wp, char* dst) {
     int qh, i;
     ql.at(wp.u, qh, i);
-    const size_t row0 = ((size_t)b * p.Hq + hk * p.G + wp.g) * N + qh * L;  // first row of the half
-    copy.issue(p.Q + row0 * D, i * BM, L, dst, 0);
-    copy.issue(p.dO + row0 * D, i * BM, L, dst, Smem::DO_OFF);
-    if (w == 0) async_load_row_floats(p.lse2 + row0, i * BM, L, reinterpret_cast<float*>(dst + Smem::LSE_OFF), lane);
-    if (w == 1) async_load_row_floats(p.delta + row0, i * BM, L, reinterpret_cast<float*>(dst + Smem::DLT_OFF), lane);
+    const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
+    const int row0 = qh * L + i * BM;
+    copy.issue(p.Q + hrow * D, N, row0, dst);
+    copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
+    // (copy.wave is uniform: a scalar branch, so the buffer descriptors stay scalar)
+    if (copy.wave == 0)
+      async_load_row_floats(p.lse2 + hrow, N, row0, reinterpret_cast<float*>(dst + Smem::LSE_OFF), lane);
+    if (copy.wave == 1)
+      async_load_row_floats(p.delta + hrow, N, row0, reinterpret_cast<float*>(dst + Smem::DLT_OFF), lane);
   };
   WalkPos cur = {0, 0};
   if (per_g > 0) cur = {t0 / per_g, t0 % per_g};
@@ -371,9 +376,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   auto issue = [&](int t, char* kdst, char* vdst) {
     int kh, j;
     kl.at(t, kh, j);
-    const size_t hb = kvbase + (size_t)kh * L * D;
-    copy.issue(p.K + hb, j * BN, L, kdst, 0);
-    copy.issue(p.V + hb, j * BN, L, vdst, 0);
+    copy.issue(p.K + kvbase, N, kh * L + j * BN, kdst);
+    copy.issue(p.V + kvbase, N, kh * L + j * BN, vdst);
   };
   if (T > 0) issue(0, lds, lds + 2 * TILE);
 

@@ -168,26 +168,33 @@ __device__ inline bf16x8 lds_tr(const char* lds, uint32_t b0, uint32_t b1, int c
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Asynchronous copy of a tile of NR rows x D bf16 from a row-major global
-// array into a swizzled LDS tile with global_load_lds (16 bytes per lane, the
-// LDS address of lane i is M0 + 16*i).  Each wave instruction fills 1 KiB of
-// the tile contiguously; lane i fetches the global chunk that belongs at LDS
-// chunk p (the XOR swizzle is its own inverse).  The per-lane byte offsets of
-// those chunks do not depend on which tile is copied, so they are computed
-// once; a whole tile then costs one scalar base per instruction.  Rows past
-// nrows are clamped to the last row: the kernels mask them out, so they only
-// need finite data.  Completion is tracked by the wave's vmcnt
-// (wait_global_loads) and must be followed by a workgroup barrier before
-// other waves read the tile.
+// Buffer resource over `bytes` bytes at base (raw buffer, no stride): loads
+// at offsets at or past `bytes` return zero instead of faulting.
+__device__ inline __amdgpu_buffer_rsrc_t make_buffer(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+// Asynchronous copy of a tile of NR rows x D bf16 from a row-major array into
+// a swizzled LDS tile with buffer_load ... lds (16 bytes per lane; the LDS
+// address of lane i is M0 + 16*i).  Each wave instruction fills 1 KiB of the
+// tile contiguously; lane i fetches the global chunk that belongs at LDS chunk
+// p (the XOR swizzle is its own inverse).  The per-lane byte offsets do not
+// depend on which tile is copied, so a copy costs one scalar buffer
+// descriptor per tile.  Rows past the end of the array read as zero; rows
+// past the end of a half read the other half's rows: the kernels mask both out.
+//
+// Buffer (MUBUF) rather than global (FLAT-encoded) loads: the compiler
+// treats a FLAT load into LDS as touching both counters, and while one is in
+// flight it turns every LDS-read wait into a full drain (lgkmcnt(0)), which
+// would serialise the operand reads of the whole step behind the prefetch.
+// Completion is tracked by the wave's vmcnt (wait_global_loads) and must be
+// followed by a workgroup barrier before other waves read the tile.
 template <int D, int NR, int NT>
 struct TileCopy {
   static constexpr int CPR = D / 8;
   static constexpr int NW = NT / 64;
   static constexpr int NI = NR * CPR / NT;
   static_assert(NI * NT == NR * CPR, "tile must split evenly over the workgroup");
-  // (The source addresses are passed to the builtin as const void*: with a
-  // const char* argument the host compilation pass silently dropped the launch
-  // stub of one kernel using this copy.)
   uint32_t boff[NI];  // byte offset of the source chunk from the tile's first row
   int wave;           // wave index, uniform
   __device__ explicit TileCopy(int tid) {
@@ -200,63 +207,24 @@ struct TileCopy {
       boff[u] = (uint32_t)(2 * (row * D + (((p % CPR) ^ chunk_swizzle<D>(row)) << 3)));
     }
   }
-  // Copy rows [row0, row0 + NR) of src (clamped to < nrows) into the tile at
-  // LDS byte offset tile_off of lds (a multiple of 1 KiB).
-  __device__ void issue(const bf16* src, int row0, int nrows, char* lds, uint32_t tile_off) const {
-    const char* base = reinterpret_cast<const char*>(src + (size_t)row0 * D);
-    if (row0 + NR <= nrows) {
+  // Copy rows [row0, row0 + NR) of the row-major array arr[nrows][D] into
+  // the tile at dst.  The buffer starts at row0 (the range check covers the
+  // per-lane offset only), so rows at or past nrows read as zero.
+  __device__ void issue(const bf16* arr, int nrows, int row0, char* dst) const {
+    const __amdgpu_buffer_rsrc_t rsrc = make_buffer(arr + (size_t)row0 * D, (uint32_t)((nrows - row0) * D * 2));
 #pragma unroll
-      for (int u = 0; u < NI; ++u)
-        __builtin_amdgcn_global_load_lds((const void*)(base + boff[u]),
-                                         (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + wave) * 1024),
-                                         16, 0, 0);
-    } else {
-#pragma unroll
-      for (int u = 0; u < NI; ++u) {
-        const int row = (int)(boff[u] / (2 * D));
-        const int over = imax(0, row0 + row - (nrows - 1));  // rows to step back
-        __builtin_amdgcn_global_load_lds((const void*)(base + boff[u] - (size_t)over * 2 * D),
-                                         (__attribute__((address_space(3))) void*)(lds + tile_off + (u * NW + wave) * 1024),
-                                         16, 0, 0);
-      }
-    }
+    for (int u = 0; u < NI; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc, (__attribute__((address_space(3))) void*)(dst + (u * NW + wave) * 1024), 16, (int)boff[u], 0, 0, 0);
   }
 };
 
-// Asynchronous copy of NR rows starting at row0 of a row-major bf16 array
-// [nrows][D] into a swizzled LDS tile [NR][D] (global_load_lds_dwordx4).  Each
-// wave instruction fills 1 KiB of LDS contiguously, 16 bytes per lane in lane
-// order; lane i fetches the global chunk that belongs at LDS chunk p (the XOR
-// swizzle is its own inverse).  Rows past nrows are clamped to the last row:
-// the kernels mask them out, so they only need finite data.  Completion is
-// tracked by the wave's vmcnt (wait_global_loads) and must be followed by a
-// workgroup barrier before other waves read the tile.
-template <int D, int NR, int NT>
-__device__ inline void async_load_tile(const bf16* src, int row0, int nrows, bf16* tile, int tid) {
-  constexpr int CPR = D / 8;            // 16-byte chunks per row
-  constexpr int NW = NT / 64;           // waves in the workgroup
-  constexpr int NI = NR * CPR / NT;     // instructions per wave
-  static_assert(NI * NT == NR * CPR, "tile must split evenly over the workgroup");
-  const int w = tid >> 6, lane = tid & 63;
-#pragma unroll
-  for (int u = 0; u < NI; ++u) {
-    const int blk = u * NW + w;         // 1 KiB block of the tile filled by this instruction
-    const int p = blk * 64 + lane;      // LDS chunk written by this lane
-    const int row = p / CPR;
-    const int chunk = (p % CPR) ^ chunk_swizzle<D>(row);
-    const int r = imin(row0 + row, nrows - 1);
-    __builtin_amdgcn_global_load_lds(src + (size_t)r * D + chunk * 8,
-                                     (__attribute__((address_space(3))) void*)(tile + blk * 512), 16, 0, 0);
-  }
+// Asynchronous copy of 64 consecutive floats arr[row0 .. row0+63] (those at or
+// past nrows read as zero) into LDS dst[0..63]: one instruction of one wave.
+__device__ inline void async_load_row_floats(const float* arr, int nrows, int row0, float* dst, int lane) {
+  const __amdgpu_buffer_rsrc_t rsrc = make_buffer(arr + row0, (uint32_t)((nrows - row0) * 4));
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)dst, 4, 4 * lane, 0, 0, 0);
 }
-
-// Asynchronous copy of 64 consecutive floats src[row0 .. row0+63] (indices
-// clamped to < nrows) into LDS dst[0..63]: one instruction of one wave.
-__device__ inline void async_load_row_floats(const float* src, int row0, int nrows, float* dst, int lane) {
-  const int r = imin(row0 + lane, nrows - 1);
-  __builtin_amdgcn_global_load_lds(src + r, (__attribute__((address_space(3))) void*)dst, 4, 0, 0);
-}
-
 
 __device__ inline u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 

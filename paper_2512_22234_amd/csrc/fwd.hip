@@ -90,12 +90,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
+  // K and V of this (batch, KV head): 2L rows each
   auto issue = [&](int t, char* kdst, char* vdst) {
     int kh, j;
     kl.at(t, kh, j);
-    const size_t hb = kvbase + (size_t)kh * L * D;
-    copy.issue(p.K + hb, j * BN, L, kdst, 0);
-    copy.issue(p.V + hb, j * BN, L, vdst, 0);
+    copy.issue(p.K + kvbase, N, kh * L + j * BN, kdst);
+    copy.issue(p.V + kvbase, N, kh * L + j * BN, vdst);
   };
 
   if (T > 0) issue(0, lds, lds + 2 * TILE);

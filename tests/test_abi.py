@@ -141,6 +141,7 @@ def _bwd(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(D=96), 2), (dict(D=256), 2), (dict(dtype=3), 2),
     (dict(Hq=3, Hkv=2), 1), (dict(B=0), 1), (dict(L=0), 1), (dict(S=0), 1),
+    (dict(L=(1 << 22) + 1), 1),            # beyond 32-bit buffer offsets of one head
     (dict(Q=0), 1), (dict(O=0), 1), (dict(LSE=0), 1), (dict(ws=0), 1),
     (dict(Q=A + 8), 1), (dict(O=A + 3 * SZ + 2), 1), (dict(LSE=A + 4 * SZ + 2), 1),
     (dict(O=A + 16), 1),                   # output overlaps Q
@@ -156,7 +157,7 @@ def test_fwd_validation(kw, status):
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(D=32), 2), (dict(Hq=4, Hkv=3), 1), (dict(dO=0), 1), (dict(dV=0), 1),
+    (dict(D=32), 2), (dict(Hq=4, Hkv=3), 1), (dict(dO=0), 1), (dict(dV=0), 1), (dict(L=(1 << 22) + 1), 1),
     (dict(dQ=A + SZ + 16), 1),             # dQ overlaps Q
     (dict(dK=A + 6 * SZ + 64), 1),         # dK overlaps dQ
     (dict(dV=A + 5 * SZ), 1),              # dV overlaps LSE
