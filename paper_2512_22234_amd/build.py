@@ -30,12 +30,14 @@ CFLAGS = [
 ]
 
 
-# Per-file additions.  The forward kernel: no NaN semantics (its inputs are
-# finite or -inf, so fmax needs no quieting of its operands), and MFMAs in
-# their VGPR form (the scores are consumed by VALU code, so AGPR accumulators
-# would be copied back every tile).
+# Per-file additions.  MFMAs in their VGPR form: scores and score gradients
+# are consumed by VALU code, so AGPR accumulators would be copied back every
+# tile (the long-lived dK/dV accumulators are pinned to AGPRs explicitly).
+# The forward kernel also drops NaN semantics (its inputs are finite or -inf,
+# so fmax needs no quieting of its operands).
 FILE_FLAGS = {
     "fwd.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -155,25 +155,30 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int T = t1 - t0;
 
   const TileCopy<D, BM, 256> copy(tid);
-  // Q, dO, lse2 and delta of one query head (2L rows each)
-  auto issue = [&](WalkPos wp, char* dst) {
+  // Q, dO, lse2 and delta of one query head (2L rows each).  Even waves copy
+  // the lse2 row and odd waves the delta row (each twice, the same data), so
+  // the copy is branch-free and its buffer descriptors stay scalar.
+  auto issue = [&](WalkPos wp, char* dst, int part) {
     int qh, i;
     ql.at(wp.u, qh, i);
     const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
     const int row0 = qh * L + i * BM;
-    copy.issue(p.Q + hrow * D, N, row0, dst);
-    copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
-    // (copy.wave is uniform: a scalar branch, so the buffer descriptors stay scalar)
-    if (copy.wave == 0)
-      async_load_row_floats(p.lse2 + hrow, N, row0, reinterpret_cast<float*>(dst + Smem::LSE_OFF), lane);
-    if (copy.wave == 1)
-      async_load_row_floats(p.delta + hrow, N, row0, reinterpret_cast<float*>(dst + Smem::DLT_OFF), lane);
+    if (part == 0) {
+      copy.issue(p.Q + hrow * D, N, row0, dst);
+      const bool odd = (copy.wave & 1) != 0;
+      async_load_row_floats((odd ? p.delta : p.lse2) + hrow, N, row0,
+                            reinterpret_cast<float*>(dst + (odd ? Smem::DLT_OFF : Smem::LSE_OFF)), lane);
+    } else {
+      copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
+    }
   };
+  constexpr int NI = decltype(copy)::NI;  // vector-memory instructions per tile copy
   WalkPos cur = {0, 0};
   if (per_g > 0) cur = {t0 / per_g, t0 % per_g};
   WalkPos nxt = cur;
   if (T > 0) {
-    issue(cur, sm.buf[0]);
+    issue(cur, sm.buf[0], 0);
+    issue(cur, sm.buf[0], 1);
     nxt.next(per_g);
   }
 
@@ -200,22 +205,26 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   // every LDS access let the compiler see that the copy in flight cannot
   // overwrite the tile being read, so it does not wait for the copy before
   // the reads (the wait at the end of the step covers it).
+  //
+  // The copy of the next tile is spread between the step's MFMAs (a CU
+  // accepts vector memory requests at a limited rate, so a burst at the top
+  // would stall the wave).  The last step copies its own tile again, into the
+  // buffer nothing reads afterwards, so the step is straight-line code.
   auto tile_step = [&](const char* __restrict__ bc, char* __restrict__ bn, int t) __attribute__((always_inline)) {
     const char* bd = bc + Smem::DO_OFF;
-    if (t + 1 < T) {
-      issue(nxt, bn);
-      nxt.next(per_g);
-    }
+    const WalkPos src = t + 1 < T ? nxt : cur;
+    nxt.next(per_g);
     int qh, i;
     ql.at(cur.u, qh, i);
     cur.next(per_g);
     const int q0 = i * BM, q1 = imin(L, q0 + BM);
+    // (EMPTY tiles are never visited; the window test would mask all of one)
     const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
-    if (cls != TILE_EMPTY) {
+    {
       // query q0 + offset sees this lane's key iff win.lo <= q0 + offset < win.hi
       const PosWindow win = queries_seeing(kh, qh, kblock0, L, S, kvalid);
-      const unsigned span = cls == TILE_PARTIAL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
-      const int rel = cls == TILE_PARTIAL ? q0 + 4 * g2 - win.lo : 0;
+      const unsigned span = cls != TILE_FULL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
+      const int rel = cls != TILE_FULL ? q0 + 4 * g2 - win.lo : 0;
       // one 32-query block at a time keeps S, dP, P and dS of a single block live
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
@@ -230,6 +239,12 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
         for (int s = 0; s < DS; ++s) {
           sacc = mfma32(lds_rows<D>(bc, ops.row_rel, s, qb), kreg[s], sacc);
           dpacc = mfma32(lds_rows<D>(bd, ops.row_rel, s, qb), vreg[s], dpacc);
+        }
+        // one part of the next tile's copy, spread between these MFMAs
+        if (qb < 2) {
+          issue(src, bn, qb);
+          if (qb == 0) interleave_copies<2 * DS, NI + 1, 0>();
+          else interleave_copies<2 * DS, NI, 1>();
         }
 #pragma unroll
         for (int i4 = 0; i4 < 4; ++i4) {
@@ -379,6 +394,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     copy.issue(p.K + kvbase, N, kh * L + j * BN, kdst);
     copy.issue(p.V + kvbase, N, kh * L + j * BN, vdst);
   };
+  constexpr int DQ_COPIES = 2 * decltype(copy)::NI;
   if (T > 0) issue(0, lds, lds + 2 * TILE);
 
   bf16x8 qreg[DS], doreg[DS];
@@ -402,15 +418,16 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 
   // One key tile; restrict-qualified current and next buffers as in the
   // forward kernel, so the copy in flight does not make the compiler wait
-  // before the reads of the current tile.
+  // before the reads of the current tile.  The copy of the next tile is
+  // spread between the MFMAs (the last step copies its own tile again).
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
                        char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
-    if (t + 1 < T) issue(t + 1, knxt, vnxt);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
+    // (EMPTY tiles are never visited; the window test would mask all of one)
     const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
-    if (cls != TILE_EMPTY) {
+    {
       f32x16 sacc[KB], dpacc[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
@@ -419,17 +436,31 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
           sacc[kb][e] = 0.f;
           dpacc[kb][e] = 0.f;
         }
+      // the next tile's copy, one instruction per step of the loop below
+      int khn, jn;
+      kl.at(imin(t + 1, T - 1), khn, jn);
+      const __amdgpu_buffer_rsrc_t kn = decltype(copy)::rows(p.K + kvbase, N, khn * L + jn * BN);
+      const __amdgpu_buffer_rsrc_t vn = decltype(copy)::rows(p.V + kvbase, N, khn * L + jn * BN);
       // S^T[key][q] = sum_d K[key][d] Q[q][d];  dP^T[key][q] = sum_d V[key][d] dO[q][d]
 #pragma unroll
-      for (int s = 0; s < DS; ++s)
+      for (int s = 0; s < DS; ++s) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
           dpacc[kb] = mfma32(lds_rows<D>(vcur, ops.row_rel, s, kb), doreg[s], dpacc[kb]);
         }
+        constexpr int NI = decltype(copy)::NI, PER = (2 * NI + DS - 1) / DS;  // copy instructions per step
+#pragma unroll
+        for (int x = 0; x < PER; ++x) {
+          const int u = s * PER + x;
+          if (u < NI) copy.issue_one(kn, knxt, u);
+          else if (u < 2 * NI) copy.issue_one(vn, vnxt, u - NI);
+        }
+      }
+      interleave_copies<2 * DS * KB, DQ_COPIES>();
       const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
-      const unsigned span = cls == TILE_PARTIAL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
-      const int rel = cls == TILE_PARTIAL ? k0 + 4 * g2 - win.lo : 0;
+      const unsigned span = cls != TILE_FULL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
+      const int rel = cls != TILE_FULL ? k0 + 4 * g2 - win.lo : 0;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll

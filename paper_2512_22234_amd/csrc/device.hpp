@@ -207,15 +207,22 @@ struct TileCopy {
       boff[u] = (uint32_t)(2 * (row * D + (((p % CPR) ^ chunk_swizzle<D>(row)) << 3)));
     }
   }
-  // Copy rows [row0, row0 + NR) of the row-major array arr[nrows][D] into
-  // the tile at dst.  The buffer starts at row0 (the range check covers the
-  // per-lane offset only), so rows at or past nrows read as zero.
+  // Buffer over rows [row0, nrows) of the row-major array arr[nrows][D].  It
+  // starts at row0 (the range check covers the per-lane offset only), so rows
+  // at or past nrows read as zero.
+  __device__ static __amdgpu_buffer_rsrc_t rows(const bf16* arr, int nrows, int row0) {
+    return make_buffer(arr + (size_t)row0 * D, (uint32_t)((nrows - row0) * D * 2));
+  }
+  // Instruction u of the copy of the tile at the start of rsrc into dst.
+  __device__ void issue_one(__amdgpu_buffer_rsrc_t rsrc, char* dst, int u) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rsrc, (__attribute__((address_space(3))) void*)(dst + (u * NW + wave) * 1024), 16, (int)boff[u], 0, 0, 0);
+  }
+  // Copy rows [row0, row0 + NR) of arr[nrows][D] into the tile at dst.
   __device__ void issue(const bf16* arr, int nrows, int row0, char* dst) const {
-    const __amdgpu_buffer_rsrc_t rsrc = make_buffer(arr + (size_t)row0 * D, (uint32_t)((nrows - row0) * D * 2));
+    const __amdgpu_buffer_rsrc_t rsrc = rows(arr, nrows, row0);
 #pragma unroll
-    for (int u = 0; u < NI; ++u)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsrc, (__attribute__((address_space(3))) void*)(dst + (u * NW + wave) * 1024), 16, (int)boff[u], 0, 0, 0);
+    for (int u = 0; u < NI; ++u) issue_one(rsrc, dst, u);
   }
 };
 
@@ -224,6 +231,21 @@ struct TileCopy {
 __device__ inline void async_load_row_floats(const float* arr, int nrows, int row0, float* dst, int lane) {
   const __amdgpu_buffer_rsrc_t rsrc = make_buffer(arr + row0, (uint32_t)((nrows - row0) * 4));
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)dst, 4, 4 * lane, 0, 0, 0);
+}
+
+// Scheduling request for the current basic block: spread NV vector-memory
+// instructions (tile copies) evenly between NM MFMAs instead of issuing them
+// as one burst.
+// Place it right after the copies, which follow the MFMAs in program order;
+// SYNC separates independent requests in one block.
+template <int NM, int NV, int SYNC = 0>
+__device__ inline void interleave_copies() {
+  static_assert(NV >= 1 && NM >= NV, "at least one MFMA per copy");
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, NM / NV, SYNC);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, SYNC);        // VMEM read
+  }
 }
 
 __device__ inline u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }

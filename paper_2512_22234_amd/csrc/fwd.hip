@@ -90,15 +90,17 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
-  // K and V of this (batch, KV head): 2L rows each
-  auto issue = [&](int t, char* kdst, char* vdst) {
+  // copy key tile t of K or V (2L rows each for this batch and KV head)
+  auto issue = [&](int t, bool is_v, char* dst) {
     int kh, j;
     kl.at(t, kh, j);
-    copy.issue(p.K + kvbase, N, kh * L + j * BN, kdst);
-    copy.issue(p.V + kvbase, N, kh * L + j * BN, vdst);
+    copy.issue((is_v ? p.V : p.K) + kvbase, N, kh * L + j * BN, dst);
   };
 
-  if (T > 0) issue(0, lds, lds + 2 * TILE);
+  if (T > 0) {
+    issue(0, false, lds);
+    issue(0, true, lds + 2 * TILE);
+  }
 
   bf16x8 qreg[DS];
   {
@@ -124,14 +126,23 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   // this gives every LDS access let the compiler see that the copy in flight
   // cannot overwrite the tiles being read, so it does not wait for the copy
   // before the reads (the wait at the end of the step covers it).
+  //
+  // The copy of the next tile is spread over the step: its K part between the
+  // score MFMAs, its V part between the PV MFMAs.  A CU accepts vector memory
+  // requests at a limited rate, so a burst of copies at the top of the step
+  // would stall the wave; spread out, each request issues while MFMAs run.
+  // The last step copies its own tile again (into the buffer nothing reads
+  // afterwards), which keeps the step straight-line code.
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
                        char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
-    if (t + 1 < T) issue(t + 1, knxt, vnxt);
+    const int tn = imin(t + 1, T - 1);
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
+    // (EMPTY tiles are never visited; were one visited, the window test of
+    // PARTIAL tiles would mask all of it)
     const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
-    if (cls != TILE_EMPTY) {
+    {
       f32x16 sacc[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
@@ -142,7 +153,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       for (int s = 0; s < DS; ++s)
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
-      if (cls == TILE_PARTIAL) {
+      issue(tn, false, knxt);
+      interleave_copies<DS * KB, decltype(copy)::NI>();
+      if (cls != TILE_FULL) {
         // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
         const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
         const unsigned span = (unsigned)(win.hi - win.lo);
@@ -195,6 +208,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, c, db), pb[c], oacc[db]);
+      issue(tn, true, vnxt);
+      interleave_copies<PC * DB, decltype(copy)::NI>();
     }
   };
   for (int t = 0; t < T; ++t) {
