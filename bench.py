@@ -3,9 +3,11 @@
 
 One step = bd_attn_fwd + bd_attn_bwd over one batch of the 8B-shaped training
 workload (B=2, Hq=32, Hkv=8, D=128, L=2048 so 4096 packed tokens, S=4, bf16
-N(0,1)*0.5 inputs, dO ~ N(0,1)), inputs resident in HBM.  W untimed warm-up
-steps, then K timed steps bracketed by device synchronisation and HIP events
-on the stream the library runs on.
+N(0,1)*0.5 inputs, dO ~ N(0,1)), inputs resident in HBM (warm caches: the
+working set fits the 256 MB Infinity Cache).  W untimed warm-up steps (10),
+then K timed steps (50) bracketed by device synchronisation and HIP events on
+the stream the library runs on; the per-step median is reported beside the
+mean.
 
 value  = effective TFLOP/s counting only visible (query, key) pairs:
          (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
@@ -135,8 +137,8 @@ def cpu_baseline(w, budget_s: float, max_groups: int):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
@@ -206,13 +208,16 @@ def main():
     ms = start.elapsed_time(end) / K
     log(f"[bench] timed region: {ms:.4f} ms/step (events), {wall * 1e3 / K:.4f} ms/step (host clock)")
 
-    # per-kernel durations from the marks
+    # per-kernel durations from the marks (mean over the timed steps), and the
+    # per-step fwd / bwd durations (median over the timed steps)
     per = {}
     for names, marks in ((fwd_names, fwd_marks), (bwd_names, bwd_marks)):
         for j, name in enumerate(names):
             per[name] = sum(m[j].elapsed_time(m[j + 1]) for m in marks) / K
     t_fwd = sum(per[n] for n in fwd_names)
     t_bwd = sum(per[n] for n in bwd_names)
+    step_ms = sorted(f[0].elapsed_time(f[-1]) + b[0].elapsed_time(b[-1]) for f, b in zip(fwd_marks, bwd_marks))
+    med_step = step_ms[len(step_ms) // 2]
 
     npairs = visible_pairs(L, S) * w.B * w.Hq
     f_fwd, f_bwd, f_bwd8 = 4 * w.D * npairs, 10 * w.D * npairs, 8 * w.D * npairs
@@ -255,7 +260,9 @@ def main():
                                f"S={S}, bf16 N(0,1)*0.5, fwd+bwd",
                    "global_batch": w.B, "seq_len": 2 * L, "parallelism": "single GPU",
                    "visible_pairs_per_head": visible_pairs(L, S),
-                   "flops_per_step": f_fwd + f_bwd, "fwd_ms": round(t_fwd, 5), "bwd_ms": round(t_bwd, 5)},
+                   "flops_per_step": f_fwd + f_bwd, "fwd_ms": round(t_fwd, 5), "bwd_ms": round(t_bwd, 5),
+                   "median_step_ms": round(med_step, 5),
+                   "fwd_tflops_eff": round(f_fwd / t_fwd / 1e9, 2), "bwd_tflops_eff": round(f_bwd / t_bwd / 1e9, 2)},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(dom, w.name), "traffic_unit": "HBM bytes per launch",

@@ -425,7 +425,6 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     int kh, j;
     kl.at(t, kh, j);
     const int k0 = j * BN, k1 = imin(L, k0 + BN);
-    // (EMPTY tiles are never visited; the window test would mask all of one)
     const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
     {
       f32x16 sacc[KB], dpacc[KB];
@@ -458,20 +457,26 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
         }
       }
       interleave_copies<2 * DS * KB, DQ_COPIES>();
+      // dS = P (dP - delta); FULL tiles without the per-element visibility test
       const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
-      const unsigned span = cls != TILE_FULL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
-      const int rel = cls != TILE_FULL ? k0 + 4 * g2 - win.lo : 0;
+      const unsigned span = (unsigned)(win.hi - win.lo);
+      const int rel = k0 + 4 * g2 - win.lo;
+      auto ds = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
+        for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const int e = 4 * i + jj;
-            float pv = fast_exp2(sacc[kb][e] * p.c - lse2);
-            pv = (unsigned)(rel + kb * 32 + 8 * i + jj) < span ? pv : 0.f;
-            sacc[kb][e] = pv * (dpacc[kb][e] - dlt);
-          }
+            for (int jj = 0; jj < 4; ++jj) {
+              const int e = 4 * i + jj;
+              float pv = fast_exp2(sacc[kb][e] * p.c - lse2);
+              if constexpr (decltype(masked)::value) pv = (unsigned)(rel + kb * 32 + 8 * i + jj) < span ? pv : 0.f;
+              sacc[kb][e] = pv * (dpacc[kb][e] - dlt);
+            }
+      };
+      // (EMPTY is never visited; it would take the masked path, which masks all of it)
+      if (cls == TILE_FULL) ds(Flag<false>());
+      else ds(Flag<true>());
       bf16x8 dsb[PC];
 #pragma unroll
       for (int c = 0; c < PC; ++c) dsb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
