@@ -17,7 +17,7 @@ constexpr int kVersion = 100;  // 0.1.0
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t delta = 0, lse2 = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
+  size_t rs = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
 };
 
 bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
@@ -32,10 +32,8 @@ Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
   const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
   size_t off = 0;
   if (bwd) {
-    w.delta = off;
-    off += align256((size_t)B * Hq * N * 4);
-    w.lse2 = off;
-    off += align256((size_t)B * Hq * N * 4);
+    w.rs = off;
+    off += align256((size_t)B * Hq * N * 8);
     w.part = off;
     off += align256(bd::dkdv_partial_floats(B, Hkv, L, D) * 4);
   }
@@ -342,13 +340,12 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
     dk = wb + w.dk;
     dv = wb + w.dv;
   }
-  float* delta = reinterpret_cast<float*>(wb + w.delta);
-  float* lse2 = reinterpret_cast<float*>(wb + w.lse2);
-  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, LSE, delta, lse2, stream));
+  float* rs = reinterpret_cast<float*>(wb + w.rs);
+  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, LSE, rs, stream));
   float* part = reinterpret_cast<float*>(wb + w.part);
-  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, lse2, delta, dk, dv, part, stream));
+  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, rs, dk, dv, part, stream));
   BD_LAUNCH(bd::launch_bwd_dkdv_combine(s, part, dk, dv, stream));
-  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, lse2, delta, dq, stream));
+  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, rs, dq, stream));
   if (dtype == BD_ATTN_FP32) {
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));

@@ -8,24 +8,26 @@
 //   dK    = scale dS^T Q                                (dkdv, key-tile major)
 //   dQ    = scale dS K                                  (dq, query-tile major)
 //
-// dkdv: a workgroup owns a (batch, KV head, 128-key tile); each of its four
-// waves owns 32 keys whose K/V rows stay in registers.  It walks the query
-// heads of the GQA group and the 64-row query tiles that can see the key tile
-// (the exact tile classification gives the list).  Scores are S = Q K^T so
-// each lane owns one key column; P and dS are then directly the B operands of
-// dV^T = dO^T P and dK^T = Q^T dS, whose A operands come from the Q and dO
-// tiles through the transposing LDS read.  Work per clean key tile shrinks
-// linearly with its position, so each clean tile's walk is split into two
-// halves run by two workgroups that write float32 partial sums; a combine
-// kernel adds the two halves in a fixed order.  Noisy key tiles (seen only by
-// their own block's noisy queries) are done by one workgroup each.
+// dkdv: a workgroup owns a (batch, KV head, 128-key tile) and walks the query
+// heads of the GQA group and the 32-row query tiles that can see the key tile
+// (the exact tile classification gives the list).  Its eight waves split the
+// work by role: four producers compute S = Q K^T and dP = dO V^T (each lane
+// owns one key column), then P and dS, and pass P and dS through LDS as bf16
+// MFMA operands; four consumers, one on each SIMD beside a producer, keep dK
+// and dV and accumulate dV^T = dO^T P and dK^T = Q^T dS, whose A operands come
+// from the Q and dO tiles through the transposing LDS read.  Work per clean
+// key tile shrinks linearly with its position, so each clean tile's walk is
+// split into two halves run by two workgroups that write float32 partial
+// sums; a combine kernel adds the two halves in a fixed order.  Noisy key
+// tiles (seen only by their own block's noisy queries) are done by one
+// workgroup each.
 //
 // dq: a workgroup owns a (batch, query head, 128-row query tile) like the
 // forward; scores are S^T = K Q^T (lane = query) and dQ^T = K^T dS^T with K^T
 // read from the K tile through the transposing LDS read.
 //
-// Tiles are copied into LDS asynchronously (global_load_lds) one step ahead,
-// double-buffered.
+// Tiles are copied into LDS asynchronously with buffer loads to LDS, ahead of
+// the step that reads them.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -33,12 +35,12 @@ namespace bd {
 namespace {
 
 // ----------------------------------------------------------------------------
-// Delta = rowsum(dO * O) and lse2 = LSE * log2(e), fp32; D/8 consecutive lanes
-// share one row.
+// (lse2, delta) = (LSE * log2(e), rowsum(dO * O)) per row, fp32, interleaved;
+// D/8 consecutive lanes share one row.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O, const bf16* __restrict__ dO,
-                                                      const float* __restrict__ LSE, float* __restrict__ delta,
-                                                      float* __restrict__ lse2, size_t rows) {
+                                                      const float* __restrict__ LSE, float* __restrict__ rs,
+                                                      size_t rows) {
   constexpr int TPR = D / 8;
   const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
   const size_t row = gid / TPR;
@@ -53,8 +55,9 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (row < rows && part == 0) {
-    delta[row] = acc;
-    lse2[row] = LSE[row] * LOG2E;
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 v = {LSE[row] * LOG2E, acc};
+    *reinterpret_cast<f32x2*>(rs + 2 * row) = v;
   }
 }
 
@@ -64,8 +67,7 @@ struct DkvParams {
   const bf16* K;
   const bf16* V;
   const bf16* dO;
-  const float* lse2;
-  const float* delta;
+  const float* rs;  // (lse2, delta) per query row
   bf16* dK;
   bf16* dV;
   float* part;  // [2 halves][2 (dK, dV)][B*Hkv][L][D] partial sums of clean key tiles
@@ -78,32 +80,20 @@ template <int D>
 struct DkvSmem {
   static constexpr int BM = DKV_BM;
   static constexpr uint32_t TILE = BM * D * 2;  // bytes per swizzled tile
-  // one contiguous region per buffer: Q tile, dO tile, lse2 and delta rows
-  static constexpr uint32_t DO_OFF = TILE, LSE_OFF = 2 * TILE, DLT_OFF = 2 * TILE + 4 * BM;
+  // one contiguous region per buffer: Q tile, dO tile, (lse2, delta) per row
+  static constexpr uint32_t DO_OFF = TILE, RS_OFF = 2 * TILE;
   static constexpr uint32_t BUF = 2 * TILE + 8 * BM;  // a multiple of 256 bytes
-  static_assert(BUF % 256 == 0, "operand addressing needs 256-byte aligned tiles");
-  alignas(256) char buf[2][BUF];
+  static constexpr int NBUF = 5;                      // copies run three steps ahead
+  // P and dS of one key group (32 keys x BM queries), as the bf16 B operands
+  // of the consumer's MFMAs: operand h of P at 2h KiB, of dS at (2h+1) KiB,
+  // 16 bytes per lane.
+  static constexpr uint32_t XGRP = 4 * BM * 32;
+  static constexpr uint32_t XBUF = 4 * XGRP;
+  static_assert(BUF % 256 == 0 && XBUF % 256 == 0, "operand addressing needs 256-byte aligned tiles");
+  static_assert(BM == 32, "one 32-query block per step");
+  alignas(256) char buf[NBUF][BUF];
+  alignas(256) char x[2][XBUF];
 };
-
-// dK/dV accumulation.  PIN keeps the accumulators in AGPRs through inline-asm
-// MFMAs (no per-iteration register copies); it is used only where the
-// compiler leaves those registers in place across the loop (D = 128; a CPU
-// test inspects the generated code), since a copy of an asm-defined
-// accumulator would not be padded for the MFMA latency.  Otherwise the
-// builtin, whose hazards the compiler tracks.
-template <bool PIN>
-__device__ inline f32x16 acc_zero() {
-  if constexpr (PIN) return mfma32_agpr_zero();
-  f32x16 z;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) z[e] = 0.f;
-  return z;
-}
-template <bool PIN>
-__device__ inline void acc_mfma(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  if constexpr (PIN) mfma32_agpr(acc, a, b);
-  else acc = mfma32(a, b, acc);
-}
 
 // Position in a head-major walk over (query head g, query tile u).
 struct WalkPos {
@@ -116,15 +106,30 @@ struct WalkPos {
   }
 };
 
+// Workgroup of eight waves on one (batch, KV head, 128-key tile).  Waves w and
+// w + 4 run on the same SIMD and share the 32 keys k0 + 32 (w % 4) + [0, 32):
+//   producer (w < 4): K and V rows of its keys in registers; S and dP of one
+//     32-query block, then P and dS, written to LDS as bf16 operands.  It is
+//     software-pipelined: step t computes P and dS of block t while the MFMAs
+//     of S and dP of block t + 1 run;
+//   consumer (w >= 4): the dK and dV accumulators; per step the two products
+//     of the block the producer finished one step earlier, and the copy of the
+//     query tile three steps ahead.
+// A producer's softmax arithmetic thus runs beside MFMAs (its own and its
+// consumer's) on the same SIMD, and each role fits the register budget of two
+// waves per SIMD.  One barrier per step.  In step t the query-tile buffers
+// hold tiles t - 1 (consumer), t and t + 1 (producer), t + 2 (landed or
+// landing) and t + 3 (being copied); the P/dS buffers steps t and t - 1.
 template <int D>
-__global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
+__global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   constexpr int BM = DKV_BM, BN = DKV_BN;
-  constexpr int DS = D / 16, DB = D / 32, QB = BM / 32;
-  constexpr bool PIN = D == 128;
+  constexpr int DS = D / 16, DB = D / 32;
   using Smem = DkvSmem<D>;
   __shared__ Smem sm;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = w & 3;  // key group
   const int l32 = lane & 31, g2 = lane >> 5;
   const int L = p.L, S = p.S, N = 2 * L;
 
@@ -142,7 +147,7 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int k0 = j * BN, k1 = imin(L, k0 + BN);
   const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
 
-  const int kk = k0 + w * 32 + l32;  // this lane's key (local to its half)
+  const int kk = k0 + kg * 32 + l32;  // this lane's key (local to its half)
   const bool kvalid = kk < k1;
   const int kblock0 = kvalid ? (kk / S) * S : 0;
   const size_t krow = (size_t)grp * N + kh * L + kk;
@@ -153,166 +158,199 @@ __global__ __launch_bounds__(256, 1) void dkdv_kernel(DkvParams p) {
   const int t0 = clean ? (split * Tall) / 2 : 0;
   const int t1 = clean ? ((split + 1) * Tall) / 2 : Tall;
   const int T = t1 - t0;
-
-  const TileCopy<D, BM, 256> copy(tid);
-  // Q, dO, lse2 and delta of one query head (2L rows each).  Even waves copy
-  // the lse2 row and odd waves the delta row (each twice, the same data), so
-  // the copy is branch-free and its buffer descriptors stay scalar.
-  auto issue = [&](WalkPos wp, char* dst, int part) {
-    int qh, i;
-    ql.at(wp.u, qh, i);
-    const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
-    const int row0 = qh * L + i * BM;
-    if (part == 0) {
-      copy.issue(p.Q + hrow * D, N, row0, dst);
-      const bool odd = (copy.wave & 1) != 0;
-      async_load_row_floats((odd ? p.delta : p.lse2) + hrow, N, row0,
-                            reinterpret_cast<float*>(dst + (odd ? Smem::DLT_OFF : Smem::LSE_OFF)), lane);
-    } else {
-      copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
-    }
-  };
-  constexpr int NI = decltype(copy)::NI;  // vector-memory instructions per tile copy
-  WalkPos cur = {0, 0};
-  if (per_g > 0) cur = {t0 / per_g, t0 % per_g};
-  WalkPos nxt = cur;
+  const int steps = T > 0 ? T + 1 : 0;  // the consumer trails the producer by one step
+  WalkPos first = {0, 0}, last = {0, 0};
   if (T > 0) {
-    issue(cur, sm.buf[0], 0);
-    issue(cur, sm.buf[0], 1);
-    nxt.next(per_g);
+    first = {t0 / per_g, t0 % per_g};
+    last = {(t1 - 1) / per_g, (t1 - 1) % per_g};
   }
-
-  bf16x8 kreg[DS], vreg[DS];
-#pragma unroll
-  for (int s = 0; s < DS; ++s) {
-    kreg[s] = kvalid ? *reinterpret_cast<const bf16x8*>(p.K + krow * D + 16 * s + 8 * g2) : zero_bf16x8();
-    vreg[s] = kvalid ? *reinterpret_cast<const bf16x8*>(p.V + krow * D + 16 * s + 8 * g2) : zero_bf16x8();
-  }
-
   const LdsOperands<D> ops(lane);
-  f32x16 dkacc[DB], dvacc[DB];
+
+  if (w < 4) {
+    // ---------------------------------------------------------------- producer
+    bf16x8 kreg[DS], vreg[DS];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dkacc[db] = acc_zero<PIN>();
-    dvacc[db] = acc_zero<PIN>();
-  }
-
-  wait_global_loads();
-  __syncthreads();
-
-  // One query tile.  The current buffer and the one the next tile is copied
-  // into are distinct restrict-qualified pointers: the alias scopes this gives
-  // every LDS access let the compiler see that the copy in flight cannot
-  // overwrite the tile being read, so it does not wait for the copy before
-  // the reads (the wait at the end of the step covers it).
-  //
-  // The copy of the next tile is spread between the step's MFMAs (a CU
-  // accepts vector memory requests at a limited rate, so a burst at the top
-  // would stall the wave).  The last step copies its own tile again, into the
-  // buffer nothing reads afterwards, so the step is straight-line code.
-  auto tile_step = [&](const char* __restrict__ bc, char* __restrict__ bn, int t) __attribute__((always_inline)) {
-    const char* bd = bc + Smem::DO_OFF;
-    const WalkPos src = t + 1 < T ? nxt : cur;
-    nxt.next(per_g);
-    int qh, i;
-    ql.at(cur.u, qh, i);
-    cur.next(per_g);
-    const int q0 = i * BM, q1 = imin(L, q0 + BM);
-    // (EMPTY tiles are never visited; the window test would mask all of one)
-    const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
-    {
-      // query q0 + offset sees this lane's key iff win.lo <= q0 + offset < win.hi
+    for (int s = 0; s < DS; ++s) {
+      kreg[s] = kvalid ? *reinterpret_cast<const bf16x8*>(p.K + krow * D + 16 * s + 8 * g2) : zero_bf16x8();
+      vreg[s] = kvalid ? *reinterpret_cast<const bf16x8*>(p.V + krow * D + 16 * s + 8 * g2) : zero_bf16x8();
+    }
+    // S[q][key] = sum_d Q[q][d] K[key][d];  dP[q][key] = sum_d dO[q][d] V[key][d]
+    auto scores = [&](const char* __restrict__ bt, f32x16& sacc, f32x16& dpacc) __attribute__((always_inline)) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        sacc[e] = 0.f;
+        dpacc[e] = 0.f;
+      }
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        sacc = mfma32(lds_rows<D>(bt, ops.row_rel, s, 0), kreg[s], sacc);
+        dpacc = mfma32(lds_rows<D>(bt + Smem::DO_OFF, ops.row_rel, s, 0), vreg[s], dpacc);
+      }
+    };
+    // P = exp2(c S - lse2), dS = P (dP - delta) of block t, into xw as bf16
+    // operands; query q0 + offset sees this lane's key iff
+    // win.lo <= q0 + offset < win.hi (FULL tiles: every query does).
+    auto softmax_grad = [&](const char* __restrict__ bt, char* __restrict__ xw, f32x16& sacc, f32x16& dpacc,
+                            int rel, unsigned span, auto masked) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int rr = 8 * i4 + 4 * g2;  // rows rr .. rr + 3 of this lane's accumulator slots
+        const f32x4 a = *reinterpret_cast<const f32x4*>(bt + Smem::RS_OFF + 8 * rr);
+        const f32x4 z = *reinterpret_cast<const f32x4*>(bt + Smem::RS_OFF + 8 * rr + 16);
+        const float l4[4] = {a[0], a[2], z[0], z[2]}, d4[4] = {a[1], a[3], z[1], z[3]};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int e = 4 * i4 + jj;
+          float pv = fast_exp2(sacc[e] * p.c - l4[jj]);
+          if constexpr (decltype(masked)::value) pv = (unsigned)(rel + 8 * i4 + jj) < span ? pv : 0.f;
+          dpacc[e] = pv * (dpacc[e] - d4[jj]);
+          sacc[e] = pv;
+        }
+      }
+      char* xg = xw + kg * Smem::XGRP + 16 * lane;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        *reinterpret_cast<bf16x8*>(xg + 2 * h * 1024) = pack8(sacc, 8 * h);
+        *reinterpret_cast<bf16x8*>(xg + (2 * h + 1) * 1024) = pack8(dpacc, 8 * h);
+      }
+    };
+    // Step t: scores of block t + 1 into (sn, dn) beside the softmax gradient
+    // of block t from (sc, dc).  Past the last block the buffer of t + 1 holds
+    // a repeated tile: its scores are computed and never used.
+    WalkPos cur = first;
+    auto step = [&](int t, f32x16& sc, f32x16& dc, f32x16& sn, f32x16& dn) __attribute__((always_inline)) {
+      int qh, i;
+      ql.at(cur.u, qh, i);
+      cur.next(per_g);
+      const int q0 = i * BM, q1 = imin(L, q0 + BM);
+      // (EMPTY tiles are never visited; the window test would mask all of one)
+      const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
       const PosWindow win = queries_seeing(kh, qh, kblock0, L, S, kvalid);
-      const unsigned span = cls != TILE_FULL ? (unsigned)(win.hi - win.lo) : 0xffffffffu;
-      const int rel = cls != TILE_FULL ? q0 + 4 * g2 - win.lo : 0;
-      // one 32-query block at a time keeps S, dP, P and dS of a single block live
+      const int rel = q0 + 4 * g2 - win.lo;
+      const unsigned span = (unsigned)(win.hi - win.lo);
+      const char* bt = sm.buf[t % Smem::NBUF];
+      const char* bn = sm.buf[(t + 1) % Smem::NBUF];
+      char* xw = sm.x[t & 1];
+      if (cls == TILE_FULL) {
+        scores(bn, sn, dn);
+        softmax_grad(bt, xw, sc, dc, rel, span, Flag<false>());
+      } else {
+        scores(bn, sn, dn);
+        softmax_grad(bt, xw, sc, dc, rel, span, Flag<true>());
+      }
+    };
+    f32x16 sA, dA, sB, dB;
+    __syncthreads();  // the first three query tiles are in LDS
+    if (T > 0) scores(sm.buf[0], sA, dA);
+    // steps alternate the two accumulator pairs (unrolled by two, no copies)
+    for (int t = 0; t < T; t += 2) {
+      step(t, sA, dA, sB, dB);
+      __syncthreads();
+      if (t + 1 < T) {
+        step(t + 1, sB, dB, sA, dA);
+        __syncthreads();
+      }
+    }
+    if (T > 0) __syncthreads();  // the consumer's last step
+  } else {
+    // ---------------------------------------------------------------- consumer
+    const TileCopy<D, BM, 256> copy(tid - 256);
+    constexpr int NC = 2 * decltype(copy)::NI + 1;  // vector-memory instructions per query-tile copy
+    // Q, dO and (lse2, delta) of one query tile.  The four waves copy the
+    // row pairs each (the same data), so every wave issues NC instructions.
+    auto issue = [&](WalkPos wp, char* dst) {
+      int qh, i;
+      ql.at(wp.u, qh, i);
+      const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
+      const int row0 = qh * L + i * BM;
+      copy.issue(p.Q + hrow * D, N, row0, dst);
+      copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
+      async_load_row_floats(p.rs + 2 * hrow, 2 * N, 2 * row0, reinterpret_cast<float*>(dst + Smem::RS_OFF), lane);
+    };
+    // tiles 0, 1 and 2 (the last tile again past the end); cp then points at tile 3
+    WalkPos cp = first;
+    if (T > 0) {
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        f32x16 sacc, dpacc;
+      for (int u = 0; u < 3; ++u) {
+        issue(u < T ? cp : last, sm.buf[u]);
+        cp.next(per_g);
+      }
+    }
+    f32x16 dkacc[DB], dvacc[DB];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          sacc[e] = 0.f;
-          dpacc[e] = 0.f;
-        }
-        // S[q][key] = sum_d Q[q][d] K[key][d];  dP[q][key] = sum_d dO[q][d] V[key][d]
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int s = 0; s < DS; ++s) {
-          sacc = mfma32(lds_rows<D>(bc, ops.row_rel, s, qb), kreg[s], sacc);
-          dpacc = mfma32(lds_rows<D>(bd, ops.row_rel, s, qb), vreg[s], dpacc);
-        }
-        // one part of the next tile's copy, spread between these MFMAs
-        if (qb < 2) {
-          issue(src, bn, qb);
-          if (qb == 0) interleave_copies<2 * DS, NI + 1, 0>();
-          else interleave_copies<2 * DS, NI, 1>();
-        }
-#pragma unroll
-        for (int i4 = 0; i4 < 4; ++i4) {
-          const int rr = qb * 32 + 8 * i4 + 4 * g2;
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(bc + Smem::LSE_OFF + 4 * rr);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(bc + Smem::DLT_OFF + 4 * rr);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            float pv = fast_exp2(sacc[4 * i4 + jj] * p.c - l4[jj]);
-            pv = (unsigned)(rel + qb * 32 + 8 * i4 + jj) < span ? pv : 0.f;
-            dpacc[4 * i4 + jj] = pv * (dpacc[4 * i4 + jj] - d4[jj]);
-            sacc[4 * i4 + jj] = pv;
-          }
-        }
+      for (int e = 0; e < 16; ++e) {
+        dkacc[db][e] = 0.f;
+        dvacc[db][e] = 0.f;
+      }
+    wait_global_loads();
+    __syncthreads();
+
+    // Step t: dV and dK from the block of step t - 1, then the copy of tile
+    // t + 3 (the last tile again past the end, into a buffer nothing reads
+    // any more, so every step issues the same copies).  The buffers read and
+    // the one written are distinct restrict-qualified pointers, so the
+    // compiler does not wait for the copy in flight before the reads.
+    auto consume = [&](const char* __restrict__ bc, const char* __restrict__ xr, char* __restrict__ bn, int t)
+                       __attribute__((always_inline)) {
+      if (t > 0) {
+        const char* xg = xr + kg * Smem::XGRP + 16 * lane;
         // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const bf16x8 pb = pack8(sacc, 8 * h), dsb = pack8(dpacc, 8 * h);
-          const int c = 2 * qb + h;
+          const bf16x8 pb = *reinterpret_cast<const bf16x8*>(xg + 2 * h * 1024);
+          const bf16x8 dsb = *reinterpret_cast<const bf16x8*>(xg + (2 * h + 1) * 1024);
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            acc_mfma<PIN>(dvacc[db], lds_tr<D>(bd, ops.tr_rel0, ops.tr_rel1, c, db), pb);
-            acc_mfma<PIN>(dkacc[db], lds_tr<D>(bc, ops.tr_rel0, ops.tr_rel1, c, db), dsb);
+            dvacc[db] = mfma32(lds_tr<D>(bc + Smem::DO_OFF, ops.tr_rel0, ops.tr_rel1, h, db), pb, dvacc[db]);
+            dkacc[db] = mfma32(lds_tr<D>(bc, ops.tr_rel0, ops.tr_rel1, h, db), dsb, dkacc[db]);
           }
         }
       }
+      issue(t + 3 < T ? cp : last, bn);
+    };
+    for (int t = 0; t < steps; ++t) {
+      consume(sm.buf[(t + Smem::NBUF - 1) % Smem::NBUF], sm.x[(t + 1) & 1], sm.buf[(t + 3) % Smem::NBUF], t);
+      if (t + 3 < T) cp.next(per_g);
+      compute_fence();
+      wait_global_loads_but<NC>();  // tile t + 2 has landed (the copy issued this step may not have)
+      __syncthreads();
     }
-  };
-  for (int t = 0; t < T; ++t) {
-    tile_step(sm.buf[t & 1], sm.buf[(t + 1) & 1], t);
-    compute_fence();
-    wait_global_loads();
-    __syncthreads();
-  }
+    wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 
-  if constexpr (PIN) mfma_drain(dkacc, dvacc);
-  if (!kvalid) return;
-  const float sc = p.scale;
-  if (clean) {
-    // float32 partial sums; the combine kernel adds the two halves
-    const size_t plane = (size_t)p.nkv * L * D;
-    float* pk = p.part + (size_t)(2 * split) * plane + ((size_t)grp * L + kk) * D + 4 * g2;
-    float* pv = pk + plane;
+    if (!kvalid) return;
+    const float sc = p.scale;
+    if (clean) {
+      // float32 partial sums; the combine kernel adds the two halves
+      const size_t plane = (size_t)p.nkv * L * D;
+      float* pk = p.part + (size_t)(2 * split) * plane + ((size_t)grp * L + kk) * D + 4 * g2;
+      float* pv = pk + plane;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const f32x4 vk = {dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc, dkacc[db][4 * i + 2] * sc,
-                          dkacc[db][4 * i + 3] * sc};
-        const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
-        *reinterpret_cast<f32x4*>(pk + db * 32 + 8 * i) = vk;
-        *reinterpret_cast<f32x4*>(pv + db * 32 + 8 * i) = vv;
-      }
-  } else {
-    bf16* dkp = p.dK + krow * D + 4 * g2;
-    bf16* dvp = p.dV + krow * D + 4 * g2;
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 vk = {dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc, dkacc[db][4 * i + 2] * sc,
+                            dkacc[db][4 * i + 3] * sc};
+          const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
+          *reinterpret_cast<f32x4*>(pk + db * 32 + 8 * i) = vk;
+          *reinterpret_cast<f32x4*>(pv + db * 32 + 8 * i) = vv;
+        }
+    } else {
+      bf16* dkp = p.dK + krow * D + 4 * g2;
+      bf16* dvp = p.dV + krow * D + 4 * g2;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        st_bf16x4(dkp + db * 32 + 8 * i, dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc,
-                  dkacc[db][4 * i + 2] * sc, dkacc[db][4 * i + 3] * sc);
-        st_bf16x4(dvp + db * 32 + 8 * i, dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2],
-                  dvacc[db][4 * i + 3]);
-      }
+        for (int i = 0; i < 4; ++i) {
+          st_bf16x4(dkp + db * 32 + 8 * i, dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc,
+                    dkacc[db][4 * i + 2] * sc, dkacc[db][4 * i + 3] * sc);
+          st_bf16x4(dvp + db * 32 + 8 * i, dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2],
+                    dvacc[db][4 * i + 3]);
+        }
+    }
   }
 }
-
 // dK/dV of the clean half = half0 + half1 (fixed order), rounded to bf16.
 // One thread per 4 consecutive features.
 __global__ __launch_bounds__(256) void dkdv_combine_kernel(const float* __restrict__ part, bf16* __restrict__ dK,
@@ -340,8 +378,7 @@ struct DqParams {
   const bf16* K;
   const bf16* V;
   const bf16* dO;
-  const float* lse2;
-  const float* delta;
+  const float* rs;  // (lse2, delta) per query row
   bf16* dQ;
   int L, S, Hq, Hkv, G, nQT, nbh;
   float c;
@@ -403,8 +440,13 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     qreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.Q + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
     doreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.dO + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
   }
-  const float lse2 = qvalid ? p.lse2[qrow] : 0.f;
-  const float dlt = qvalid ? p.delta[qrow] : 0.f;
+  float lse2 = 0.f, dlt = 0.f;
+  if (qvalid) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 r2 = *reinterpret_cast<const f32x2*>(p.rs + 2 * qrow);
+    lse2 = r2[0];
+    dlt = r2[1];
+  }
 
   const LdsOperands<D> ops(lane);
   f32x16 dqacc[DB];
@@ -509,26 +551,24 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 }
 
 template <int D>
-hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, const float* LSE, float* delta,
-                        float* lse2, hipStream_t st) {
+hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, const float* LSE, float* rs, hipStream_t st) {
   const size_t rows = (size_t)s.B * s.Hq * 2 * s.L;
   const size_t threads = rows * (D / 8);
   const dim3 grid((unsigned)((threads + 255) / 256));
   hipLaunchKernelGGL(bwd_pre_kernel<D>, grid, dim3(256), 0, st, static_cast<const bf16*>(O),
-                     static_cast<const bf16*>(dO), LSE, delta, lse2, rows);
+                     static_cast<const bf16*>(dO), LSE, rs, rows);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* lse2, const float* delta, void* dK, void* dV, float* part, hipStream_t st) {
+                         const float* rs, void* dK, void* dV, float* part, hipStream_t st) {
   DkvParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
-  p.lse2 = lse2;
-  p.delta = delta;
+  p.rs = rs;
   p.dK = static_cast<bf16*>(dK);
   p.dV = static_cast<bf16*>(dV);
   p.part = part;
@@ -542,20 +582,19 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.c = s.scale * LOG2E;
   p.scale = s.scale;
   const dim3 grid(3 * p.nKT * p.nkv);
-  hipLaunchKernelGGL(dkdv_kernel<D>, grid, dim3(256), 0, st, p);
+  hipLaunchKernelGGL(dkdv_kernel<D>, grid, dim3(512), 0, st, p);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                       const float* lse2, const float* delta, void* dQ, hipStream_t st) {
+                       const float* rs, void* dQ, hipStream_t st) {
   DqParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
-  p.lse2 = lse2;
-  p.delta = delta;
+  p.rs = rs;
   p.dQ = static_cast<bf16*>(dQ);
   p.L = s.L;
   p.S = s.S;
@@ -573,17 +612,16 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
 
 }  // namespace
 
-hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, const float* LSE, float* delta,
-                          float* lse2, hipStream_t st) {
-  if (s.D == 128) return launch_pre_d<128>(s, O, dO, LSE, delta, lse2, st);
-  return launch_pre_d<64>(s, O, dO, LSE, delta, lse2, st);
+hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, const float* LSE, float* rs,
+                          hipStream_t st) {
+  if (s.D == 128) return launch_pre_d<128>(s, O, dO, LSE, rs, st);
+  return launch_pre_d<64>(s, O, dO, LSE, rs, st);
 }
 
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                           const float* lse2, const float* delta, void* dK, void* dV, float* part,
-                           hipStream_t st) {
-  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, lse2, delta, dK, dV, part, st);
-  return launch_dkdv_d<64>(s, Q, K, V, dO, lse2, delta, dK, dV, part, st);
+                           const float* rs, void* dK, void* dV, float* part, hipStream_t st) {
+  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, rs, dK, dV, part, st);
+  return launch_dkdv_d<64>(s, Q, K, V, dO, rs, dK, dV, part, st);
 }
 
 hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, void* dV, hipStream_t st) {
@@ -597,9 +635,9 @@ hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, 
 }
 
 hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* lse2, const float* delta, void* dQ, hipStream_t st) {
-  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, lse2, delta, dQ, st);
-  return launch_dq_d<64>(s, Q, K, V, dO, lse2, delta, dQ, st);
+                         const float* rs, void* dQ, hipStream_t st) {
+  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, rs, dQ, st);
+  return launch_dq_d<64>(s, Q, K, V, dO, rs, dQ, st);
 }
 
 }  // namespace bd

@@ -44,47 +44,6 @@ __device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& 
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// The same MFMA with its accumulator pinned to AGPRs (the "+a" constraint).
-// For long-lived accumulators that only MFMAs touch inside a loop: it keeps
-// the register allocator from parking them in AGPRs between iterations and
-// copying them through VGPRs on every pass.  The compiler's hazard tracking
-// does not see inside the asm, so the two waits it would insert are explicit:
-//  - a VALU result feeding the MFMA as A or B needs two wait states; every
-//    call starts with them (s_nop 2 gives three), since the compiler may
-//    schedule the producing VALU instruction right before any of these MFMAs;
-//  - results must not be read by other instructions until mfma_drain() has
-//    run on every accumulator (it ties them as operands, so no read can be
-//    scheduled above it).
-// Back-to-back accumulation into the same registers needs no wait states.
-// The asm is not volatile: its operands carry every dependency, and a volatile
-// statement would pin the LDS reads that feed it in place (no read could be
-// hoisted above an earlier MFMA), exposing the full LDS latency on every MFMA.
-__device__ inline void mfma32_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-// A zero accumulator defined directly in AGPRs (an MFMA of zero operands), so
-// that every definition and loop use of an mfma32_agpr accumulator is AGPR.
-__device__ inline f32x16 mfma32_agpr_zero() {
-  f32x16 acc;
-  const bf16x8 z = zero_bf16x8();
-  asm volatile("s_nop 2\n v_mfma_f32_32x32x16_bf16 %0, %1, %1, 0" : "=a"(acc) : "v"(z));
-  return acc;
-}
-// 64 wait states, more than the write latency of an 8-pass MFMA, with the
-// accumulators of two arrays tied as operands so that every later read of
-// them is ordered after the wait.
-#define BD_MFMA_DRAIN_NOPS "s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7"
-template <int N>
-__device__ inline void mfma_drain(f32x16 (&x)[N], f32x16 (&y)[N]) {
-  static_assert(N == 2 || N == 4, "two or four accumulators per array");
-  if constexpr (N == 4)
-    asm volatile(BD_MFMA_DRAIN_NOPS
-                 : "+a"(x[0]), "+a"(x[1]), "+a"(x[2]), "+a"(x[3]), "+a"(y[0]), "+a"(y[1]), "+a"(y[2]), "+a"(y[3]));
-  else
-    asm volatile(BD_MFMA_DRAIN_NOPS : "+a"(x[0]), "+a"(x[1]), "+a"(y[0]), "+a"(y[1]));
-}
-#undef BD_MFMA_DRAIN_NOPS
-
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -254,6 +213,21 @@ __device__ inline void interleave_copies() {
   }
 }
 
+// Scheduling request for the current basic block: LDS operand reads run
+// AHEAD MFMAs ahead of their use.  The first AHEAD * RPM reads (plus FIRST
+// more, e.g. operands shared by all MFMAs) go first, then each MFMA is
+// followed by the RPM reads of the operand AHEAD MFMAs later.
+template <int NM, int AHEAD, int RPM, int FIRST = 0>
+__device__ inline void pipeline_lds_reads() {
+  static_assert(AHEAD >= 1 && AHEAD <= NM, "read distance");
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD * RPM + FIRST, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    if (i + AHEAD < NM) __builtin_amdgcn_sched_group_barrier(0x100, RPM, 0);
+  }
+}
+
 __device__ inline u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
 // Keeps the compiler from moving memory operations or scheduling instructions
@@ -267,6 +241,13 @@ __device__ inline void compute_fence() {
 
 // Wait until every global load this wave issued has landed (s_waitcnt vmcnt(0)).
 __device__ inline void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Wait until all but the N most recent global loads of this wave have landed
+// (loads complete in issue order for this counter).
+template <int N>
+__device__ inline void wait_global_loads_but() {
+  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
 __device__ inline void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ inline bf16x8 lds_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }

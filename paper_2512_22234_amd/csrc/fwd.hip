@@ -12,8 +12,9 @@
 // Key tiles (64 keys) are visited in the order given by the exact tile
 // classification: FULL tiles run with no per-element test, PARTIAL tiles
 // apply the visibility window per element, EMPTY tiles are never loaded.  K
-// and V tiles are copied into LDS asynchronously (global_load_lds) one tile
-// ahead, double-buffered, so the copy runs under the current tile's compute.
+// and V tiles are copied into LDS asynchronously (buffer loads to LDS) one
+// tile ahead, double-buffered, so the copy runs under the current tile's
+// compute.
 // The online softmax keeps a reference maximum per row that only moves when
 // the scores exceed it by a margin, so the O rescale is rare.
 #include "device.hpp"

@@ -1,18 +1,18 @@
-"""Static checks on the generated gfx950 code of the dK/dV kernel.
+"""Static checks on the generated gfx950 code (CPU only: hipcc cross-compiles).
 
-The D=128 dK/dV kernel keeps its accumulators in AGPRs through inline-asm
-MFMAs.  The compiler cannot see the latency of an instruction inside an asm
-statement, so two hazards are the kernel's own responsibility:
+The kernels' launch shapes depend on register and LDS budgets that only the
+compiler's output shows:
 
-  * a VALU write of an MFMA's A/B register needs two wait states before the
-    MFMA reads it;
-  * no other instruction may read or copy an accumulator register before the
-    drain (a long run of s_nop with the accumulators tied as operands) that
-    follows the last MFMA.
+  * the dK/dV kernel runs eight waves per workgroup, two per SIMD, so each
+    wave may use at most 256 registers (VGPRs and AGPRs together) or the
+    launch fails;
+  * the forward and dQ kernels are written for two 256-thread workgroups per
+    CU (same limit), and the dK/dV kernel's LDS must fit one CU's 160 KiB;
+  * no kernel may spill to scratch memory (a silent, large slowdown).
 
-This test compiles the kernel source to device assembly (CPU only) and checks
-both in program order, so a compiler change that moves or copies those
-registers fails here instead of producing wrong gradients on the GPU.
+Each source is compiled to device assembly with the library's own flags and
+the kernel metadata is checked, so a change that breaks a budget fails here
+instead of at launch time on the GPU.
 """
 from __future__ import annotations
 
@@ -26,101 +26,84 @@ import pytest
 ROOT = Path(__file__).resolve().parents[1]
 CSRC = ROOT / "paper_2512_22234_amd" / "csrc"
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-KERNEL = "_ZN2bd12_GLOBAL__N_111dkdv_kernelILi128EEEvNS0_9DkvParamsE"
+LDS_PER_CU = 160 * 1024
 
 
-def _regs(tok: str) -> set:
-    m = re.fullmatch(r"([va])\[(\d+):(\d+)\]", tok)
-    if m:
-        return {(m.group(1), r) for r in range(int(m.group(2)), int(m.group(3)) + 1)}
-    m = re.fullmatch(r"([va])(\d+)", tok)
-    return {(m.group(1), int(m.group(2)))} if m else set()
-
-
-def _kernel_instructions(asm: str, name: str):
-    lines = asm.split("\n")
-    start = next(i for i, l in enumerate(lines) if l.split(";")[0].strip() == name + ":")
-    out, in_asm = [], False
-    for l in lines[start + 1:]:
-        s = l.strip()
-        if s.startswith(";;#ASMSTART"):
-            in_asm = True
+def _metadata(asm: str) -> dict:
+    """Kernel name -> {field: int} from the AMDGPU metadata block of a .s file."""
+    out = {}
+    for block in re.split(r"\n\s+- \.", asm):
+        name = re.search(r"\.name:\s+(\S+)", block)
+        if not name or not name.group(1).startswith("_Z"):
             continue
-        if s.startswith(";;#ASMEND"):
-            in_asm = False
-            continue
-        if s.startswith(".Lfunc_end"):
-            break
-        s = s.split(";")[0].strip()
-        if not s or s.startswith(".") or s.endswith(":"):
-            continue
-        parts = s.replace(",", " ").split()
-        out.append((parts[0], parts[1:], in_asm))
+        fields = {}
+        for key in ("vgpr_count", "agpr_count", "sgpr_count", "private_segment_fixed_size",
+                    "group_segment_fixed_size"):
+            m = re.search(r"\.?" + key + r":\s+(\d+)", "." + block)
+            if m:
+                fields[key] = int(m.group(1))
+        out[name.group(1)] = fields
     return out
 
 
-def _hazards(insts):
-    problems, acc = [], set()
-    drain = None
-    for k, (op, args, in_asm) in enumerate(insts):
-        if in_asm and op.startswith("v_mfma") and args[0].startswith("a"):
-            acc |= _regs(args[0])
-            srcs = _regs(args[1]) | _regs(args[2])
-            waits = 0
-            for kk in range(k - 1, -1, -1):  # two wait states back
-                if waits >= 2:
-                    break
-                op2, args2, _ = insts[kk]
-                if op2.startswith("v_") and not op2.startswith("v_mfma") and args2 and _regs(args2[0]) & srcs:
-                    problems.append(f"VALU write {op2} {args2[0]} feeds an asm MFMA within 2 wait states")
-                waits += int(args2[0], 0) + 1 if op2 == "s_nop" else 1
-        if in_asm and op == "s_nop" and args[0] == "7":
-            drain = k
-    assert acc, "no AGPR-pinned MFMAs found"
-    assert drain is not None, "no drain found"
-    for k, (op, args, in_asm) in enumerate(insts):
-        if in_asm or k > drain:
-            continue
-        touched = set().union(*(_regs(a) for a in args)) if args else set()
-        if touched & acc:
-            problems.append(f"{op} {' '.join(args)} touches an accumulator before the drain")
-    return problems, len(acc)
-
-
 @pytest.fixture(scope="module")
-def dkdv_asm(tmp_path_factory):
+def kernels(tmp_path_factory):
     if not Path(HIPCC).exists():
         pytest.skip("hipcc not available")
     from paper_2512_22234_amd.build import compile_flags
-    out = tmp_path_factory.mktemp("isa") / "bwd.s"
-    flags = [f for f in compile_flags("bwd.hip") if f != "-fPIC"]
-    cmd = [HIPCC, *flags, f"-I{CSRC}", "--cuda-device-only", "-S", "-o", str(out), str(CSRC / "bwd.hip")]
-    r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
-    assert r.returncode == 0, r.stderr[-2000:]
-    return out.read_text()
+    meta = {}
+    for src in ("fwd.hip", "bwd.hip"):
+        out = tmp_path_factory.mktemp("isa") / (src + ".s")
+        flags = [f for f in compile_flags(src) if f != "-fPIC"]
+        cmd = [HIPCC, *flags, f"-I{CSRC}", "--cuda-device-only", "-S", "-o", str(out), str(CSRC / src)]
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+        assert r.returncode == 0, r.stderr[-2000:]
+        meta.update(_metadata(out.read_text()))
+    return meta
 
 
-def test_dkdv_agpr_accumulators_hazard_free(dkdv_asm):
-    problems, n = _hazards(_kernel_instructions(dkdv_asm, KERNEL))
-    assert n == 128, n  # 4 dK + 4 dV accumulators of 16 registers
-    assert not problems, problems[:10]
+def _find(meta, part):
+    found = {k: v for k, v in meta.items() if part in k}
+    assert found, f"no kernel matching {part}"
+    return found
 
 
-def test_checker_flags_early_read():
-    """The checker itself: a copy of an accumulator before the drain, and a VALU
-    write right before an asm MFMA, are both reported."""
+def test_no_scratch_spills(kernels):
+    assert len(kernels) >= 9
+    for name, f in kernels.items():
+        assert f.get("private_segment_fixed_size", 0) == 0, name
+
+
+@pytest.mark.parametrize("part", ["dkdv_kernelILi128", "dkdv_kernelILi64", "fwd_kernelILi128",
+                                  "fwd_kernelILi64", "dq_kernelILi128", "dq_kernelILi64"])
+def test_two_waves_per_simd_fit(kernels, part):
+    for name, f in _find(kernels, part).items():
+        # gfx950 metadata: vgpr_count counts architectural VGPRs, agpr_count the
+        # accumulation registers; a wave's allocation is their sum (each rounded
+        # to 8), and two waves share a SIMD's 512
+        total = -(-f["vgpr_count"] // 8) * 8 + -(-f.get("agpr_count", 0) // 8) * 8
+        assert total <= 256, (name, f)
+
+
+def test_dkdv_lds_fits_one_cu(kernels):
+    for name, f in _find(kernels, "dkdv_kernel").items():
+        assert 0 < f["group_segment_fixed_size"] <= LDS_PER_CU, (name, f)
+
+
+def test_metadata_parser():
     asm = "\n".join([
-        "k:",
-        ";;#ASMSTART", "v_mfma_f32_32x32x16_bf16 a[0:15], v[0:3], v[4:7], a[0:15]", ";;#ASMEND",
-        "v_accvgpr_read_b32 v20, a3",
-        "v_cvt_pk_bf16_f32 v4, v8, v9",
-        ";;#ASMSTART", "v_mfma_f32_32x32x16_bf16 a[0:15], v[0:3], v[4:7], a[0:15]", ";;#ASMEND",
-        ";;#ASMSTART", "s_nop 7", ";;#ASMEND",
-        "v_accvgpr_read_b32 v21, a4",
-        "s_endpgm",
-        ".Lfunc_end0:",
+        "amdhsa.kernels:",
+        "  - .agpr_count:     4",
+        "    .group_segment_fixed_size: 1024",
+        "    .name:           _Zfoo",
+        "    .private_segment_fixed_size: 16",
+        "    .sgpr_count:     20",
+        "    .vgpr_count:     100",
+        "  - .agpr_count:     0",
+        "    .name:           _Zbar",
+        "    .vgpr_count:     12",
     ])
-    problems, _ = _hazards(_kernel_instructions(asm, "k"))
-    assert any("before the drain" in p for p in problems)
-    assert any("feeds an asm MFMA" in p for p in problems)
-    assert len(problems) == 2
+    m = _metadata(asm)
+    assert m["_Zfoo"] == {"vgpr_count": 100, "agpr_count": 4, "sgpr_count": 20,
+                          "private_segment_fixed_size": 16, "group_segment_fixed_size": 1024}
+    assert m["_Zbar"]["vgpr_count"] == 12 and m["_Zbar"]["agpr_count"] == 0
