@@ -17,7 +17,7 @@ constexpr int kVersion = 100;  // 0.1.0
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t rs = 0, part = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
+  size_t rs = 0, part = 0, pair = 0, q = 0, k = 0, v = 0, o = 0, dout = 0, dq = 0, dk = 0, dv = 0, total = 0;
 };
 
 bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
@@ -36,6 +36,8 @@ Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
     off += align256((size_t)B * Hq * N * 8);
     w.part = off;
     off += align256(bd::dkdv_partial_floats(B, Hkv, L, D) * 4);
+    w.pair = off;
+    off += align256(bd::dkdv_pair_ints(B, Hkv, L) * 4);
   }
   if (dtype == BD_ATTN_FP32) {
     w.q = off; off += align256(nq * 2);
@@ -243,9 +245,9 @@ int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void*
 
 const char* bd_attn_stage_names(int for_bwd, int dtype) {
   if (dtype == BD_ATTN_FP32)
-    return for_bwd ? "cast_q,cast_k,cast_v,cast_o,cast_do,bwd_pre,bwd_dkdv,bwd_dkdv_combine,bwd_dq,cast_dq,cast_dk,cast_dv"
+    return for_bwd ? "cast_q,cast_k,cast_v,cast_o,cast_do,bwd_dq,bwd_dkdv,cast_dq,cast_dk,cast_dv"
                    : "cast_q,cast_k,cast_v,fwd,cast_o";
-  return for_bwd ? "bwd_pre,bwd_dkdv,bwd_dkdv_combine,bwd_dq" : "fwd";
+  return for_bwd ? "bwd_dq,bwd_dkdv" : "fwd";
 }
 
 }  // extern "C"
@@ -341,11 +343,10 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
     dv = wb + w.dv;
   }
   float* rs = reinterpret_cast<float*>(wb + w.rs);
-  BD_LAUNCH(bd::launch_bwd_pre(s, o, g, LSE, rs, stream));
   float* part = reinterpret_cast<float*>(wb + w.part);
-  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, rs, dk, dv, part, stream));
-  BD_LAUNCH(bd::launch_bwd_dkdv_combine(s, part, dk, dv, stream));
-  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, rs, dq, stream));
+  int* pair = reinterpret_cast<int*>(wb + w.pair);
+  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, o, LSE, rs, pair, dq, stream));
+  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, rs, dk, dv, part, pair, stream));
   if (dtype == BD_ATTN_FP32) {
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
     BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));

@@ -1,12 +1,13 @@
 // Backward pass of block-diffusion masked attention for gfx950: the
 // vector-Jacobian product of softmax attention under the mask of Eq. 1 / Eq. 2
-// (DiRL Section 4.1), with no atomics, so results are bitwise reproducible.
+// (DiRL Section 4.1), with no floating-point atomics, so results are bitwise
+// reproducible.
 //
-//   Delta = rowsum(dO * O), lse2 = LSE * log2(e)        (bwd_pre)
+//   Delta = rowsum(dO * O), lse2 = LSE * log2(e)        (dq prologue)
 //   P     = exp2(scale*log2(e) * Q K^T - lse2) on visible pairs
 //   dV    = P^T dO,  dP = dO V^T,  dS = P * (dP - Delta)
+//   dQ    = scale dS K                                  (dq, query-tile major; runs first)
 //   dK    = scale dS^T Q                                (dkdv, key-tile major)
-//   dQ    = scale dS K                                  (dq, query-tile major)
 //
 // dkdv: a workgroup owns a (batch, KV head, 128-key tile) and walks the query
 // heads of the GQA group and the 32-row query tiles that can see the key tile
@@ -17,14 +18,17 @@
 // and dV and accumulate dV^T = dO^T P and dK^T = Q^T dS, whose A operands come
 // from the Q and dO tiles through the transposing LDS read.  Work per clean
 // key tile shrinks linearly with its position, so each clean tile's walk is
-// split into two halves run by two workgroups that write float32 partial
-// sums; a combine kernel adds the two halves in a fixed order.  Noisy key
-// tiles (seen only by their own block's noisy queries) are done by one
-// workgroup each.
+// split into two halves run by two workgroups.  Whichever half finishes first
+// leaves its float32 sums in the workspace; the other adds them to its own and
+// writes dK/dV.  Float addition of two terms commutes, so the result does not
+// depend on which half finishes first.  Noisy key tiles (seen only by their
+// own block's noisy queries) are done by one workgroup each.
 //
 // dq: a workgroup owns a (batch, query head, 128-row query tile) like the
 // forward; scores are S^T = K Q^T (lane = query) and dQ^T = K^T dS^T with K^T
-// read from the K tile through the transposing LDS read.
+// read from the K tile through the transposing LDS read.  Its prologue also
+// computes Delta and lse2 of its rows for the dK/dV kernel, and the kernel
+// clears the counters with which the dK/dV kernel pairs its split walks.
 //
 // Tiles are copied into LDS asynchronously with buffer loads to LDS, ahead of
 // the step that reads them.
@@ -35,33 +39,6 @@ namespace bd {
 namespace {
 
 // ----------------------------------------------------------------------------
-// (lse2, delta) = (LSE * log2(e), rowsum(dO * O)) per row, fp32, interleaved;
-// D/8 consecutive lanes share one row.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const bf16* __restrict__ O, const bf16* __restrict__ dO,
-                                                      const float* __restrict__ LSE, float* __restrict__ rs,
-                                                      size_t rows) {
-  constexpr int TPR = D / 8;
-  const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const size_t row = gid / TPR;
-  const int part = (int)(gid % TPR);
-  float acc = 0.f;
-  if (row < rows) {
-    const bf16x8 o = *reinterpret_cast<const bf16x8*>(O + row * D + part * 8);
-    const bf16x8 g = *reinterpret_cast<const bf16x8*>(dO + row * D + part * 8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc += (float)o[e] * (float)g[e];
-  }
-#pragma unroll
-  for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (row < rows && part == 0) {
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 v = {LSE[row] * LOG2E, acc};
-    *reinterpret_cast<f32x2*>(rs + 2 * row) = v;
-  }
-}
-
-// ----------------------------------------------------------------------------
 struct DkvParams {
   const bf16* Q;
   const bf16* K;
@@ -70,7 +47,8 @@ struct DkvParams {
   const float* rs;  // (lse2, delta) per query row
   bf16* dK;
   bf16* dV;
-  float* part;  // [2 halves][2 (dK, dV)][B*Hkv][L][D] partial sums of clean key tiles
+  float* part;  // [2 (dK, dV)][B*Hkv][L][D]: unscaled sums of the half of a clean key tile's walk that finished first
+  int* pair;    // per (clean key tile, key group): arrival count and ready flag, zeroed by the dq kernel
   int L, S, Hq, Hkv, G, nKT, nkv;
   float c;      // scale * log2(e)
   float scale;
@@ -319,24 +297,71 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     }
     wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 
-    if (!kvalid) return;
     const float sc = p.scale;
     if (clean) {
-      // float32 partial sums; the combine kernel adds the two halves
+      // The two halves of this key tile's walk meet here, per key group: the
+      // first to arrive stores its float32 sums and raises the ready flag;
+      // the second waits for the flag (the first is running, since it has
+      // arrived), adds those sums to its own and writes dK/dV.  a + b == b + a
+      // in floating point, so the output does not depend on the order; the
+      // sums are stored unscaled and dK is scaled after the addition, so no
+      // multiply-add can fuse one side's product into the sum.
+      //
+      // The sums and the flag are written and read with device-scope (sc1)
+      // accesses, which the L2 of one XCD does not hold back from another,
+      // and the sums are complete (vmcnt) before the flag is stored.  Cache-wide
+      // release/acquire fences would instead write back and invalidate the
+      // whole L2 under the workgroups still running.
+      int* cnt = p.pair + 2 * ((j * p.nkv + grp) * 4 + kg);
+      int* ready = cnt + 1;
       const size_t plane = (size_t)p.nkv * L * D;
-      float* pk = p.part + (size_t)(2 * split) * plane + ((size_t)grp * L + kk) * D + 4 * g2;
-      float* pv = pk + plane;
+      const float* pbase = p.part + (size_t)grp * L * D;  // this KV head's rows, dK plane
+      const __amdgpu_buffer_rsrc_t pk = make_buffer(pbase, (uint32_t)(L * D * 4));
+      const __amdgpu_buffer_rsrc_t pv = make_buffer(pbase + plane, (uint32_t)(L * D * 4));
+      const uint32_t poff = (uint32_t)((kk * D + 4 * g2) * 4);
+      constexpr int SC1 = 16;  // cache-policy bit: device scope
+      int order = 0;
+      if (lane == 0) order = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      order = __builtin_amdgcn_readfirstlane(order);
+      if (order == 0) {
+        if (kvalid) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const f32x4 vk = {dkacc[db][4 * i], dkacc[db][4 * i + 1], dkacc[db][4 * i + 2], dkacc[db][4 * i + 3]};
+              const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
+              __builtin_amdgcn_raw_buffer_store_b128(vk, pk, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+              __builtin_amdgcn_raw_buffer_store_b128(vv, pv, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the sums have reached device scope
+        if (lane == 0) __hip_atomic_store(ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+      // Bounded wait (the first half is past its last step and only stores
+      // its sums); the bound only guarantees that the wave always ends.
+      for (int spin = 0; spin < (1 << 22); ++spin) {
+        if (__hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      asm volatile("" ::: "memory");
+      if (!kvalid) return;
+      bf16* dkp = p.dK + krow * D + 4 * g2;
+      bf16* dvp = p.dV + krow * D + 4 * g2;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const f32x4 vk = {dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc, dkacc[db][4 * i + 2] * sc,
-                            dkacc[db][4 * i + 3] * sc};
-          const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
-          *reinterpret_cast<f32x4*>(pk + db * 32 + 8 * i) = vk;
-          *reinterpret_cast<f32x4*>(pv + db * 32 + 8 * i) = vv;
+          const f32x4 ok = __builtin_amdgcn_raw_buffer_load_b128(pk, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+          const f32x4 ov = __builtin_amdgcn_raw_buffer_load_b128(pv, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+          st_bf16x4(dkp + db * 32 + 8 * i, (dkacc[db][4 * i] + ok[0]) * sc, (dkacc[db][4 * i + 1] + ok[1]) * sc,
+                    (dkacc[db][4 * i + 2] + ok[2]) * sc, (dkacc[db][4 * i + 3] + ok[3]) * sc);
+          st_bf16x4(dvp + db * 32 + 8 * i, dvacc[db][4 * i] + ov[0], dvacc[db][4 * i + 1] + ov[1],
+                    dvacc[db][4 * i + 2] + ov[2], dvacc[db][4 * i + 3] + ov[3]);
         }
     } else {
+      if (!kvalid) return;
       bf16* dkp = p.dK + krow * D + 4 * g2;
       bf16* dvp = p.dV + krow * D + 4 * g2;
 #pragma unroll
@@ -351,26 +376,6 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     }
   }
 }
-// dK/dV of the clean half = half0 + half1 (fixed order), rounded to bf16.
-// One thread per 4 consecutive features.
-__global__ __launch_bounds__(256) void dkdv_combine_kernel(const float* __restrict__ part, bf16* __restrict__ dK,
-                                                           bf16* __restrict__ dV, int nkv, int L, int D) {
-  const size_t plane = (size_t)nkv * L * D;
-  const size_t quads = plane / 4;
-  const size_t stride = (size_t)gridDim.x * 256;
-  for (size_t qd = (size_t)blockIdx.x * 256 + threadIdx.x; qd < quads; qd += stride) {
-    const size_t e = qd * 4;
-    const size_t row = e / D;  // grp * L + key
-    const size_t grp = row / L, key = row - grp * L;
-    const size_t out = ((grp * 2 + 1) * L + key) * D + (e - row * D);
-    const f32x4 k0 = *reinterpret_cast<const f32x4*>(part + e);
-    const f32x4 v0 = *reinterpret_cast<const f32x4*>(part + plane + e);
-    const f32x4 k1 = *reinterpret_cast<const f32x4*>(part + 2 * plane + e);
-    const f32x4 v1 = *reinterpret_cast<const f32x4*>(part + 3 * plane + e);
-    st_bf16x4(dK + out, k0[0] + k1[0], k0[1] + k1[1], k0[2] + k1[2], k0[3] + k1[3]);
-    st_bf16x4(dV + out, v0[0] + v1[0], v0[1] + v1[1], v0[2] + v1[2], v0[3] + v1[3]);
-  }
-}
 
 // ----------------------------------------------------------------------------
 struct DqParams {
@@ -378,7 +383,11 @@ struct DqParams {
   const bf16* K;
   const bf16* V;
   const bf16* dO;
-  const float* rs;  // (lse2, delta) per query row
+  const bf16* O;
+  const float* LSE;
+  float* rs;  // out: (lse2, delta) per query row, for the dK/dV kernel
+  int* pair;  // dK/dV pairing counters, cleared here
+  int npair;
   bf16* dQ;
   int L, S, Hq, Hkv, G, nQT, nbh;
   float c;
@@ -435,18 +444,23 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   if (T > 0) issue(0, lds, lds + 2 * TILE);
 
   bf16x8 qreg[DS], doreg[DS];
+  float dlt = 0.f;  // Delta = rowsum(dO * O); each half-wave holds half of the row's features
 #pragma unroll
   for (int s = 0; s < DS; ++s) {
     qreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.Q + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
     doreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(p.dO + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
+    const bf16x8 o = qvalid ? *reinterpret_cast<const bf16x8*>(p.O + qrow * D + 16 * s + 8 * g2) : zero_bf16x8();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dlt += (float)doreg[s][e] * (float)o[e];
   }
-  float lse2 = 0.f, dlt = 0.f;
-  if (qvalid) {
+  dlt = halves_sum(dlt);
+  const float lse2 = qvalid ? p.LSE[qrow] * LOG2E : 0.f;
+  if (qvalid && g2 == 0) {
     typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 r2 = *reinterpret_cast<const f32x2*>(p.rs + 2 * qrow);
-    lse2 = r2[0];
-    dlt = r2[1];
+    const f32x2 v = {lse2, dlt};
+    *reinterpret_cast<f32x2*>(p.rs + 2 * qrow) = v;
   }
+  for (int i = id * 256 + tid; i < p.npair; i += gridDim.x * 256) p.pair[i] = 0;
 
   const LdsOperands<D> ops(lane);
   f32x16 dqacc[DB];
@@ -551,18 +565,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 }
 
 template <int D>
-hipError_t launch_pre_d(const Shape& s, const void* O, const void* dO, const float* LSE, float* rs, hipStream_t st) {
-  const size_t rows = (size_t)s.B * s.Hq * 2 * s.L;
-  const size_t threads = rows * (D / 8);
-  const dim3 grid((unsigned)((threads + 255) / 256));
-  hipLaunchKernelGGL(bwd_pre_kernel<D>, grid, dim3(256), 0, st, static_cast<const bf16*>(O),
-                     static_cast<const bf16*>(dO), LSE, rs, rows);
-  return hipGetLastError();
-}
-
-template <int D>
 hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* rs, void* dK, void* dV, float* part, hipStream_t st) {
+                         const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st) {
   DkvParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
@@ -572,6 +576,7 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.dK = static_cast<bf16*>(dK);
   p.dV = static_cast<bf16*>(dV);
   p.part = part;
+  p.pair = pair;
   p.L = s.L;
   p.S = s.S;
   p.Hq = s.Hq;
@@ -587,14 +592,18 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
 }
 
 template <int D>
-hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                       const float* rs, void* dQ, hipStream_t st) {
+hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO, const void* O,
+                       const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st) {
   DqParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
   p.V = static_cast<const bf16*>(V);
   p.dO = static_cast<const bf16*>(dO);
+  p.O = static_cast<const bf16*>(O);
+  p.LSE = LSE;
   p.rs = rs;
+  p.pair = pair;
+  p.npair = (int)dkdv_pair_ints(s.B, s.Hkv, s.L);
   p.dQ = static_cast<bf16*>(dQ);
   p.L = s.L;
   p.S = s.S;
@@ -612,32 +621,16 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
 
 }  // namespace
 
-hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, const float* LSE, float* rs,
-                          hipStream_t st) {
-  if (s.D == 128) return launch_pre_d<128>(s, O, dO, LSE, rs, st);
-  return launch_pre_d<64>(s, O, dO, LSE, rs, st);
-}
-
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                           const float* rs, void* dK, void* dV, float* part, hipStream_t st) {
-  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, rs, dK, dV, part, st);
-  return launch_dkdv_d<64>(s, Q, K, V, dO, rs, dK, dV, part, st);
+                           const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st) {
+  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, rs, dK, dV, part, pair, st);
+  return launch_dkdv_d<64>(s, Q, K, V, dO, rs, dK, dV, part, pair, st);
 }
 
-hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, void* dV, hipStream_t st) {
-  const int nkv = s.B * s.Hkv;
-  const size_t quads = (size_t)nkv * s.L * s.D / 4;
-  size_t blocks = (quads + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(dkdv_combine_kernel, dim3((unsigned)blocks), dim3(256), 0, st, part, static_cast<bf16*>(dK),
-                     static_cast<bf16*>(dV), nkv, s.L, s.D);
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* rs, void* dQ, hipStream_t st) {
-  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, rs, dQ, st);
-  return launch_dq_d<64>(s, Q, K, V, dO, rs, dQ, st);
+hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO, const void* O,
+                         const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st) {
+  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st);
+  return launch_dq_d<64>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st);
 }
 
 }  // namespace bd

@@ -275,6 +275,17 @@ __device__ inline void st_bf16x4(bf16* p, float a, float b, float c, float d) {
   *reinterpret_cast<bf16x4*>(p) = v;
 }
 
+// Combine a per-lane value over the two half-waves (lanes l and l + 32 hold
+// the two halves of one row's keys or features) with v_permlane32_swap.
+__device__ inline float halves_max(float x) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+__device__ inline float halves_sum(float x) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+}
+
 // Workgroup -> head mapping that keeps all query heads of one KV group on the
 // same XCD (workgroups are dispatched round-robin over the 8 XCDs), so K/V of a
 // group are shared through that XCD's L2.  pos in [0, nbh); falls back to the

@@ -47,17 +47,6 @@ struct FwdSmem {
 // reference).
 constexpr float RESCALE_SLACK = 8.0f;
 
-// Combine a per-lane value over the two half-waves (lanes l and l + 32 hold
-// the two halves of one query row's keys) with v_permlane32_swap.
-__device__ inline float halves_max(float x) {
-  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-}
-__device__ inline float halves_sum(float x) {
-  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-}
-
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   constexpr int BM = FWD_BM, BN = FWD_BN;

@@ -26,22 +26,27 @@ hipError_t launch_cast_bf16_to_f32(const void* x, float* y, size_t n, hipStream_
 hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* V,
                       void* O, float* LSE, hipStream_t st);
 
-// Per query row the float32 pair (lse2, delta) = (LSE * log2(e), rowsum(dO * O)),
-// interleaved: rs[2 * row], rs[2 * row + 1]; B*Hq*2L rows.
-hipError_t launch_bwd_pre(const Shape& s, const void* O, const void* dO, const float* LSE, float* rs,
-                          hipStream_t st);
-// dK/dV kernel: noisy key tiles straight to dK/dV, clean key tiles as two
-// float32 partial sums in part (dkdv_partial_floats elements), which the
-// combine kernel then adds into dK/dV.
+// Backward, in launch order:
+//   dq:   dQ, and per query row the float32 pair (lse2, delta) =
+//         (LSE * log2(e), rowsum(dO * O)) interleaved in rs[2 * row], rs[2 * row + 1]
+//         (B*Hq*2L rows); also zeroes the dK/dV pairing counters `pair`.
+//   dkdv: dK and dV.  Each clean key tile's walk runs as two halves; the half
+//         that finishes first leaves float32 sums in `part` (dkdv_partial_floats
+//         elements), the other adds them to its own.
+hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
+                         const void* O, const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st);
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V,
-                           const void* dO, const float* rs, void* dK, void* dV, float* part, hipStream_t st);
-hipError_t launch_bwd_dkdv_combine(const Shape& s, const float* part, void* dK, void* dV, hipStream_t st);
-hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V,
-                         const void* dO, const float* rs, void* dQ, hipStream_t st);
+                           const void* dO, const float* rs, void* dK, void* dV, float* part, int* pair,
+                           hipStream_t st);
 
-// float32 partial sums of the clean half of dK and dV: 2 halves x 2 tensors.
+// float32 sums of one half of the clean key tiles' walks: dK and dV.
 inline size_t dkdv_partial_floats(int B, int Hkv, int L, int D) {
-  return (size_t)4 * B * Hkv * L * D;
+  return (size_t)2 * B * Hkv * L * D;
+}
+// Pairing counters: per (clean key tile, batch x KV head, key group of 32) an
+// arrival count and a ready flag.
+inline size_t dkdv_pair_ints(int B, int Hkv, int L) {
+  return (size_t)2 * 4 * B * Hkv * ((L + DKV_BN - 1) / DKV_BN);
 }
 
 }  // namespace bd

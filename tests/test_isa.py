@@ -69,7 +69,7 @@ def _find(meta, part):
 
 
 def test_no_scratch_spills(kernels):
-    assert len(kernels) >= 9
+    assert len(kernels) >= 6  # fwd, dkdv, dq at D = 64 and 128
     for name, f in kernels.items():
         assert f.get("private_segment_fixed_size", 0) == 0, name
 
