@@ -178,18 +178,27 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
     }
   } else {
     for (int c = 0; c < nk; ++c) {
-      const int kh = c / nkt, k0 = (c % nkt) * BN, k1 = bd::imin(L, k0 + BN);
+      const int kh = c / nkt, j = c % nkt, k0 = j * BN, k1 = bd::imin(L, k0 + BN);
       const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
-      const bd::QueryTileList ql = bd::query_tiles_for_key_tile(kh, c % nkt, L, S, BM, BN);
-      for (int t = 0; t < ql.count(); ++t) {
-        int qh, i;
-        ql.at(t, qh, i);
-        if (i < 0 || i >= nqt) return BD_ATTN_ERR_INVALID_ARGUMENT;
-        const int q0 = i * BM, q1 = bd::imin(L, q0 + BM);
-        const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
-        const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
-        const int fast = bd::classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, full);
-        out[(size_t)(qh * nqt + i) * nk + c] += (int8_t)(fast == ref ? 1 : 64);
+      // the walks of the workgroups that own this key tile, as the kernel
+      // takes them (one query head: the kernel repeats each (tile, half)
+      // once per head of the group)
+      for (int split = 0; split < 2; ++split) {
+        const bd::QueryWalk wk = bd::query_walk(kh, j, split, L, S, BM, BN, 1);
+        bd::WalkPos pos = wk.first(), prev = pos;
+        for (int t = 0; t < wk.steps(); ++t, pos.next(wk)) {
+          prev = pos;
+          const int qh = pos.qh, i = pos.tile(wk);
+          if (i < 0 || i >= nqt) return BD_ATTN_ERR_INVALID_ARGUMENT;
+          const int q0 = i * BM, q1 = bd::imin(L, q0 + BM);
+          const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
+          const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
+          const int fast = bd::classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, full);
+          out[(size_t)(qh * nqt + i) * nk + c] += (int8_t)(fast == ref ? 1 : 64);
+        }
+        // the kernel repeats the last position's copy past the end of the walk
+        const bd::WalkPos l = wk.last();
+        if (wk.steps() > 0 && (l.k != prev.k || l.qh != prev.qh || l.g != prev.g)) return BD_ATTN_ERR_INVALID_ARGUMENT;
       }
     }
   }

@@ -73,17 +73,6 @@ struct DkvSmem {
   alignas(256) char x[2][XBUF];
 };
 
-// Position in a head-major walk over (query head g, query tile u).
-struct WalkPos {
-  int g, u;
-  __device__ void next(int per_g) {
-    if (++u == per_g) {
-      u = 0;
-      ++g;
-    }
-  }
-};
-
 // Workgroup of eight waves on one (batch, KV head, 128-key tile).  Waves w and
 // w + 4 run on the same SIMD and share the 32 keys k0 + 32 (w % 4) + [0, 32):
 //   producer (w < 4): K and V rows of its keys in registers; S and dP of one
@@ -95,7 +84,8 @@ struct WalkPos {
 //     query tile three steps ahead.
 // A producer's softmax arithmetic thus runs beside MFMAs (its own and its
 // consumer's) on the same SIMD, and each role fits the register budget of two
-// waves per SIMD.  One barrier per step.  In step t the query-tile buffers
+// waves per SIMD.  One barrier per step; it drains LDS operations only, so the
+// copies issued in a step stay in flight across it.  In step t the query-tile buffers
 // hold tiles t - 1 (consumer), t and t + 1 (producer), t + 2 (landed or
 // landing) and t + 3 (being copied); the P/dS buffers steps t and t - 1.
 template <int D>
@@ -130,18 +120,10 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int kblock0 = kvalid ? (kk / S) * S : 0;
   const size_t krow = (size_t)grp * N + kh * L + kk;
 
-  const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
-  const int per_g = ql.count();
-  const int Tall = p.G * per_g;
-  const int t0 = clean ? (split * Tall) / 2 : 0;
-  const int t1 = clean ? ((split + 1) * Tall) / 2 : Tall;
-  const int T = t1 - t0;
+  const QueryWalk wk = query_walk(kh, j, split, L, S, BM, BN, p.G);
+  const int T = wk.steps();
   const int steps = T > 0 ? T + 1 : 0;  // the consumer trails the producer by one step
-  WalkPos first = {0, 0}, last = {0, 0};
-  if (T > 0) {
-    first = {t0 / per_g, t0 % per_g};
-    last = {(t1 - 1) / per_g, (t1 - 1) % per_g};
-  }
+  const WalkPos first = wk.first(), last = wk.last();
   const LdsOperands<D> ops(lane);
 
   if (w < 4) {
@@ -197,9 +179,8 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // a repeated tile: its scores are computed and never used.
     WalkPos cur = first;
     auto step = [&](int t, f32x16& sc, f32x16& dc, f32x16& sn, f32x16& dn) __attribute__((always_inline)) {
-      int qh, i;
-      ql.at(cur.u, qh, i);
-      cur.next(per_g);
+      const int qh = cur.qh, i = cur.tile(wk);
+      cur.next(wk);
       const int q0 = i * BM, q1 = imin(L, q0 + BM);
       // (EMPTY tiles are never visited; the window test would mask all of one)
       const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
@@ -223,13 +204,13 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // steps alternate the two accumulator pairs (unrolled by two, no copies)
     for (int t = 0; t < T; t += 2) {
       step(t, sA, dA, sB, dB);
-      __syncthreads();
+      barrier_lds_only();
       if (t + 1 < T) {
         step(t + 1, sB, dB, sA, dA);
-        __syncthreads();
+        barrier_lds_only();
       }
     }
-    if (T > 0) __syncthreads();  // the consumer's last step
+    if (T > 0) barrier_lds_only();  // the consumer's last step
   } else {
     // ---------------------------------------------------------------- consumer
     const TileCopy<D, BM, 256> copy(tid - 256);
@@ -237,8 +218,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // Q, dO and (lse2, delta) of one query tile.  The four waves copy the
     // row pairs each (the same data), so every wave issues NC instructions.
     auto issue = [&](WalkPos wp, char* dst) {
-      int qh, i;
-      ql.at(wp.u, qh, i);
+      const int qh = wp.qh, i = wp.tile(wk);
       const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
       const int row0 = qh * L + i * BM;
       copy.issue(p.Q + hrow * D, N, row0, dst);
@@ -251,7 +231,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
 #pragma unroll
       for (int u = 0; u < 3; ++u) {
         issue(u < T ? cp : last, sm.buf[u]);
-        cp.next(per_g);
+        cp.next(wk);
       }
     }
     f32x16 dkacc[DB], dvacc[DB];
@@ -290,10 +270,10 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     };
     for (int t = 0; t < steps; ++t) {
       consume(sm.buf[(t + Smem::NBUF - 1) % Smem::NBUF], sm.x[(t + 1) & 1], sm.buf[(t + 3) % Smem::NBUF], t);
-      if (t + 3 < T) cp.next(per_g);
+      if (t + 3 < T) cp.next(wk);
       compute_fence();
       wait_global_loads_but<NC>();  // tile t + 2 has landed (the copy issued this step may not have)
-      __syncthreads();
+      barrier_lds_only();           // ... in every wave's part; the copy in flight stays in flight
     }
     wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 

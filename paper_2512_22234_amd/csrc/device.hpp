@@ -249,6 +249,19 @@ __device__ inline void wait_global_loads_but() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
 
+// Workgroup barrier that drains this wave's LDS operations (lgkmcnt(0)) but
+// not its global loads.  __syncthreads() would also wait for every global
+// load in flight (vmcnt(0)), including tile copies issued for steps well
+// ahead; a kernel that uses this barrier waits for the copies it needs with
+// wait_global_loads_but<N>() first.  The signal fences keep the compiler from
+// moving memory operations across it.
+__device__ inline void barrier_lds_only() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima (no wait)
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ inline void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ inline bf16x8 lds_bf16x8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 // 8 consecutive elements (one 16-byte chunk) of a swizzled tile; col % 8 == 0.

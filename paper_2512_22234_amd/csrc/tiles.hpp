@@ -193,4 +193,64 @@ BD_HD QueryTileList query_tiles_for_key_tile(int kh, int j, int L, int S, int BM
   return r;
 }
 
+// The query tiles one dK/dV workgroup visits for its key tile: tiles
+// u0 + du*k, k = 0 .. K-1; each of the first K2 tiles is visited in its noisy
+// and then its clean half, the others in half `rest` only, and every (tile,
+// half) once per query head of the GQA group (G of them), heads innermost.
+struct WalkPos;
+struct QueryWalk {
+  int u0, du, K, K2, rest, G;
+  BD_HD int steps() const { return G * (K + K2); }
+  BD_HD WalkPos first() const;
+  BD_HD WalkPos last() const;
+};
+// Position (walk tile k, half qh, query head g) in a QueryWalk.
+struct WalkPos {
+  int k, qh, g;
+  BD_HD void next(const QueryWalk& wk) {
+    if (++g < wk.G) return;
+    g = 0;
+    if (qh == HALF_NOISY && k < wk.K2) {
+      qh = HALF_CLEAN;
+      return;
+    }
+    ++k;
+    qh = k < wk.K2 ? HALF_NOISY : wk.rest;
+  }
+  BD_HD int tile(const QueryWalk& wk) const { return wk.u0 + wk.du * k; }
+};
+BD_HD WalkPos QueryWalk::first() const { return WalkPos{0, K2 > 0 ? HALF_NOISY : rest, 0}; }
+BD_HD WalkPos QueryWalk::last() const {
+  return K > K2 ? WalkPos{K - 1, rest, G - 1} : WalkPos{K2 - 1, HALF_CLEAN, G - 1};
+}
+
+// Walk of key tile (kh, j).  A clean key tile is seen by noisy query tiles
+// [noisy0, nQT) and clean ones [clean0, nQT), clean0 <= noisy0; it is done by
+// two workgroups (split 0 and 1) whose walks take alternate tiles from the
+// top down, so they have equal work to within one tile.  A noisy key tile is
+// seen by noisy query tiles [noisy0, noisy0 + nnoisy) only and is done by one
+// workgroup (split 0).  Walks start at the highest tile and move down, heads
+// innermost, so the workgroups of all key tiles of one KV group read the same
+// query tile at about the same time.
+BD_HD QueryWalk query_walk(int kh, int j, int split, int L, int S, int BM, int BN, int G) {
+  const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
+  QueryWalk wk;
+  wk.G = G;
+  if (kh == HALF_CLEAN) {
+    const int nQT = ql.clean0 + ql.nclean;
+    wk.u0 = nQT - 1 - split;
+    wk.du = -2;
+    wk.K = wk.u0 >= ql.clean0 ? (wk.u0 - ql.clean0) / 2 + 1 : 0;
+    wk.K2 = (ql.nnoisy > 0 && wk.u0 >= ql.noisy0) ? imin(wk.K, (wk.u0 - ql.noisy0) / 2 + 1) : 0;
+    wk.rest = HALF_CLEAN;
+  } else {
+    wk.u0 = ql.noisy0 + ql.nnoisy - 1;
+    wk.du = -1;
+    wk.K = split == 0 ? ql.nnoisy : 0;
+    wk.K2 = 0;
+    wk.rest = HALF_NOISY;
+  }
+  return wk;
+}
+
 }  // namespace bd

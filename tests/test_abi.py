@@ -73,7 +73,9 @@ def test_classifier_matches_explicit_mask(L, S, BM, BN):
     np.testing.assert_array_equal(got, want)
 
 
-@pytest.mark.parametrize("L,S,BM,BN", CASES[1::3] + [(2048, 4, 128, 64), (2048, 4, 64, 128), (8192, 4, 128, 64)])
+@pytest.mark.parametrize("L,S,BM,BN", CASES[1::3] + [(2048, 4, 128, 64), (2048, 4, 64, 128), (8192, 4, 128, 64),
+                                                    (2048, 4, 32, 128), (2048, 64, 32, 128), (300, 5, 32, 128),
+                                                    (33, 40, 32, 128), (1, 1, 32, 128)])
 def test_tile_walks_visit_each_nonempty_pair_once(L, S, BM, BN):
     cls = bd.bd_attn_classify_tiles_host(L, S, BM, BN)
     for by_key in (False, True):
