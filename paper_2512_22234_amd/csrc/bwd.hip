@@ -213,6 +213,12 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     if (T > 0) barrier_lds_only();  // the consumer's last step
   } else {
     // ---------------------------------------------------------------- consumer
+    // Consumer c = w - 4 owns one tensor (dV for c < 2, dK for c >= 2) of the
+    // 64 keys k0 + 64 (c % 2) + [0, 64), i.e. key groups 2 (c % 2) and
+    // 2 (c % 2) + 1: every dO^T or Q^T operand it reads serves two MFMAs.
+    const int c = w - 4;
+    const bool isdk = c >= 2;
+    const int kc0 = k0 + 64 * (c & 1);
     const TileCopy<D, BM, 256> copy(tid - 256);
     constexpr int NC = 2 * decltype(copy)::NI + 1;  // vector-memory instructions per query-tile copy
     // Q, dO and (lse2, delta) of one query tile.  The four waves copy the
@@ -234,39 +240,47 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
         cp.next(wk);
       }
     }
-    f32x16 dkacc[DB], dvacc[DB];
+    f32x16 acc[2][DB];  // [key group of 32][feature block of 32]
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        dkacc[db][e] = 0.f;
-        dvacc[db][e] = 0.f;
-      }
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[ks][db][e] = 0.f;
     wait_global_loads();
     __syncthreads();
 
-    // Step t: dV and dK from the block of step t - 1, then the copy of tile
+    // Step t: the products of the block of step t - 1, then the copy of tile
     // t + 3 (the last tile again past the end, into a buffer nothing reads
     // any more, so every step issues the same copies).  The buffers read and
     // the one written are distinct restrict-qualified pointers, so the
     // compiler does not wait for the copy in flight before the reads.
+    //   dV^T[d][key] += sum_q dO^T[d][q] P[q][key]   (dV consumers)
+    //   dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]   (dK consumers)
+    const uint32_t aoff = isdk ? 0u : Smem::DO_OFF;  // A operand: Q^T or dO^T
+    const int xsel = isdk ? 1 : 0;                   // B operand: dS or P
     auto consume = [&](const char* __restrict__ bc, const char* __restrict__ xr, char* __restrict__ bn, int t)
                        __attribute__((always_inline)) {
       if (t > 0) {
-        const char* xg = xr + kg * Smem::XGRP + 16 * lane;
-        // dV^T[d][key] += sum_q dO^T[d][q] P[q][key];  dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]
+        bf16x8 xb[2][2];  // [key group][16-query half]
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const bf16x8 pb = *reinterpret_cast<const bf16x8*>(xg + 2 * h * 1024);
-          const bf16x8 dsb = *reinterpret_cast<const bf16x8*>(xg + (2 * h + 1) * 1024);
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            xb[ks][h] = *reinterpret_cast<const bf16x8*>(xr + (2 * (c & 1) + ks) * Smem::XGRP + 16 * lane +
+                                                         (2 * h + xsel) * 1024);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            dvacc[db] = mfma32(lds_tr<D>(bc + Smem::DO_OFF, ops.tr_rel0, ops.tr_rel1, h, db), pb, dvacc[db]);
-            dkacc[db] = mfma32(lds_tr<D>(bc, ops.tr_rel0, ops.tr_rel1, h, db), dsb, dkacc[db]);
+            const bf16x8 a = lds_tr<D>(bc + aoff, ops.tr_rel0, ops.tr_rel1, h, db);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) acc[ks][db] = mfma32(a, xb[ks][h], acc[ks][db]);
           }
-        }
+        issue(t + 3 < T ? cp : last, bn);
+      } else {
+        issue(t + 3 < T ? cp : last, bn);
       }
-      issue(t + 3 < T ? cp : last, bn);
     };
     for (int t = 0; t < steps; ++t) {
       consume(sm.buf[(t + Smem::NBUF - 1) % Smem::NBUF], sm.x[(t + 1) & 1], sm.buf[(t + 3) % Smem::NBUF], t);
@@ -277,43 +291,47 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     }
     wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 
-    const float sc = p.scale;
+    const float sc = isdk ? p.scale : 1.f;
+    bf16* const outp = isdk ? p.dK : p.dV;
+    const size_t orow = (size_t)grp * N + kh * L;  // first row of this KV head's half
     if (clean) {
-      // The two halves of this key tile's walk meet here, per key group: the
-      // first to arrive stores its float32 sums and raises the ready flag;
-      // the second waits for the flag (the first is running, since it has
-      // arrived), adds those sums to its own and writes dK/dV.  a + b == b + a
-      // in floating point, so the output does not depend on the order; the
-      // sums are stored unscaled and dK is scaled after the addition, so no
-      // multiply-add can fuse one side's product into the sum.
+      // The two halves of this key tile's walk meet here, per consumer wave:
+      // the first to arrive stores its float32 sums and raises the ready
+      // flag; the second waits for the flag (the first is running, since it
+      // has arrived), adds those sums to its own and writes its tensor.
+      // a + b == b + a in floating point, so the output does not depend on
+      // the order; the sums are stored unscaled and dK is scaled after the
+      // addition, so no multiply-add can fuse one side's product into the sum.
       //
       // The sums and the flag are written and read with device-scope (sc1)
       // accesses, which the L2 of one XCD does not hold back from another,
       // and the sums are complete (vmcnt) before the flag is stored.  Cache-wide
       // release/acquire fences would instead write back and invalidate the
       // whole L2 under the workgroups still running.
-      int* cnt = p.pair + 2 * ((j * p.nkv + grp) * 4 + kg);
+      int* cnt = p.pair + 2 * ((j * p.nkv + grp) * 4 + c);
       int* ready = cnt + 1;
       const size_t plane = (size_t)p.nkv * L * D;
-      const float* pbase = p.part + (size_t)grp * L * D;  // this KV head's rows, dK plane
-      const __amdgpu_buffer_rsrc_t pk = make_buffer(pbase, (uint32_t)(L * D * 4));
-      const __amdgpu_buffer_rsrc_t pv = make_buffer(pbase + plane, (uint32_t)(L * D * 4));
-      const uint32_t poff = (uint32_t)((kk * D + 4 * g2) * 4);
+      const float* pbase = p.part + (isdk ? 0 : plane) + (size_t)grp * L * D;  // this KV head's rows
+      const __amdgpu_buffer_rsrc_t pr = make_buffer(pbase, (uint32_t)(L * D * 4));
       constexpr int SC1 = 16;  // cache-policy bit: device scope
       int order = 0;
       if (lane == 0) order = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       order = __builtin_amdgcn_readfirstlane(order);
       if (order == 0) {
-        if (kvalid) {
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
+        for (int ks = 0; ks < 2; ++ks) {
+          const int key = kc0 + 32 * ks + l32;
+          if (key < k1) {
+            const uint32_t poff = (uint32_t)((key * D + 4 * g2) * 4);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const f32x4 vk = {dkacc[db][4 * i], dkacc[db][4 * i + 1], dkacc[db][4 * i + 2], dkacc[db][4 * i + 3]};
-              const f32x4 vv = {dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2], dvacc[db][4 * i + 3]};
-              __builtin_amdgcn_raw_buffer_store_b128(vk, pk, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-              __builtin_amdgcn_raw_buffer_store_b128(vv, pv, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-            }
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const f32x4 v = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
+                                 acc[ks][db][4 * i + 3]};
+                __builtin_amdgcn_raw_buffer_store_b128(v, pr, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+              }
+          }
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the sums have reached device scope
         if (lane == 0) __hip_atomic_store(ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -326,33 +344,36 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
         __builtin_amdgcn_s_sleep(2);
       }
       asm volatile("" ::: "memory");
-      if (!kvalid) return;
-      bf16* dkp = p.dK + krow * D + 4 * g2;
-      bf16* dvp = p.dV + krow * D + 4 * g2;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+      for (int ks = 0; ks < 2; ++ks) {
+        const int key = kc0 + 32 * ks + l32;
+        if (key < k1) {
+          const uint32_t poff = (uint32_t)((key * D + 4 * g2) * 4);
+          bf16* op = outp + (orow + key) * D + 4 * g2;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x4 ok = __builtin_amdgcn_raw_buffer_load_b128(pk, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-          const f32x4 ov = __builtin_amdgcn_raw_buffer_load_b128(pv, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-          st_bf16x4(dkp + db * 32 + 8 * i, (dkacc[db][4 * i] + ok[0]) * sc, (dkacc[db][4 * i + 1] + ok[1]) * sc,
-                    (dkacc[db][4 * i + 2] + ok[2]) * sc, (dkacc[db][4 * i + 3] + ok[3]) * sc);
-          st_bf16x4(dvp + db * 32 + 8 * i, dvacc[db][4 * i] + ov[0], dvacc[db][4 * i + 1] + ov[1],
-                    dvacc[db][4 * i + 2] + ov[2], dvacc[db][4 * i + 3] + ov[3]);
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const f32x4 o = __builtin_amdgcn_raw_buffer_load_b128(pr, poff + 4 * (db * 32 + 8 * i), 0, SC1);
+              st_bf16x4(op + db * 32 + 8 * i, (acc[ks][db][4 * i] + o[0]) * sc, (acc[ks][db][4 * i + 1] + o[1]) * sc,
+                        (acc[ks][db][4 * i + 2] + o[2]) * sc, (acc[ks][db][4 * i + 3] + o[3]) * sc);
+            }
         }
+      }
     } else {
-      if (!kvalid) return;
-      bf16* dkp = p.dK + krow * D + 4 * g2;
-      bf16* dvp = p.dV + krow * D + 4 * g2;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+      for (int ks = 0; ks < 2; ++ks) {
+        const int key = kc0 + 32 * ks + l32;
+        if (key < k1) {
+          bf16* op = outp + (orow + key) * D + 4 * g2;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          st_bf16x4(dkp + db * 32 + 8 * i, dkacc[db][4 * i] * sc, dkacc[db][4 * i + 1] * sc,
-                    dkacc[db][4 * i + 2] * sc, dkacc[db][4 * i + 3] * sc);
-          st_bf16x4(dvp + db * 32 + 8 * i, dvacc[db][4 * i], dvacc[db][4 * i + 1], dvacc[db][4 * i + 2],
-                    dvacc[db][4 * i + 3]);
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              st_bf16x4(op + db * 32 + 8 * i, acc[ks][db][4 * i] * sc, acc[ks][db][4 * i + 1] * sc,
+                        acc[ks][db][4 * i + 2] * sc, acc[ks][db][4 * i + 3] * sc);
         }
+      }
     }
   }
 }
