@@ -114,8 +114,9 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
  * per key tile (dK/dV, by_key_tile = 1; that kernel repeats the walk for each
  * query head of the group).  A correct walk visits every non-EMPTY pair
  * exactly once.  A visited pair whose class, as the kernels compute it
- * without divisions, differs from bd_attn_classify_tiles_host's gets 64
- * instead of 1.
+ * without divisions (and the two-comparison FULL test the kernels apply
+ * per step), differs from bd_attn_classify_tiles_host's gets 64 instead
+ * of 1.
  */
 int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out);
 

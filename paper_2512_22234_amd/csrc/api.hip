@@ -164,6 +164,7 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
     for (int a = 0; a < nq; ++a) {
       const int qh = a / nqt, q0 = (a % nqt) * BM, q1 = bd::imin(L, q0 + BM);
       const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;
+      const bd::FullRange fr = bd::full_range_vs_query_tile(qh, q0, q1, L, S, BM);
       const bd::KeyTileList kl = bd::key_tiles_for_query_tile(qh, a % nqt, L, S, BM, BN);
       for (int t = 0; t < kl.count(); ++t) {
         int kh, j;
@@ -173,13 +174,15 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
         const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
         const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
         const int fast = bd::classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, full);
-        out[(size_t)a * nk + kh * nkt + j] += (int8_t)(fast == ref ? 1 : 64);
+        const bool ok = fast == ref && fr.full(kh, k0, BN) == (ref == bd::TILE_FULL);
+        out[(size_t)a * nk + kh * nkt + j] += (int8_t)(ok ? 1 : 64);
       }
     }
   } else {
     for (int c = 0; c < nk; ++c) {
       const int kh = c / nkt, j = c % nkt, k0 = j * BN, k1 = bd::imin(L, k0 + BN);
       const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
+      const bd::FullRange fr = bd::full_range_vs_key_tile(kh, k0, k1, L, S, BN);
       // the walks of the workgroups that own this key tile, as the kernel
       // takes them (one query head: the kernel repeats each (tile, half)
       // once per head of the group)
@@ -194,7 +197,8 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
           const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
           const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
           const int fast = bd::classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, full);
-          out[(size_t)(qh * nqt + i) * nk + c] += (int8_t)(fast == ref ? 1 : 64);
+          const bool ok = fast == ref && fr.full(qh, q0, BM) == (ref == bd::TILE_FULL);
+          out[(size_t)(qh * nqt + i) * nk + c] += (int8_t)(ok ? 1 : 64);
         }
         // the kernel repeats the last position's copy past the end of the walk
         const bd::WalkPos l = wk.last();

@@ -113,7 +113,6 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int split = clean ? (rank & 1) : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
   const int k0 = j * BN, k1 = imin(L, k0 + BN);
-  const int kA = (k0 / S) * S, kB = ((k1 - 1) / S) * S;
 
   const int kk = k0 + kg * 32 + l32;  // this lane's key (local to its half)
   const bool kvalid = kk < k1;
@@ -176,26 +175,31 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     };
     // Step t: scores of block t + 1 into (sn, dn) beside the softmax gradient
     // of block t from (sc, dc).  Past the last block the buffer of t + 1 holds
-    // a repeated tile: its scores are computed and never used.
+    // a repeated tile: its scores are computed and never used.  The per-step
+    // bookkeeping is kept to a few scalar instructions: the FULL test is two
+    // comparisons against per-workgroup bounds, the visibility windows of
+    // both halves are computed once, and the buffers rotate by offset.
+    const FullRange fr = full_range_vs_key_tile(kh, k0, k1, L, S, BN);
+    const PosWindow win_n = queries_seeing(kh, HALF_NOISY, kblock0, L, S, kvalid);
+    const PosWindow win_c = queries_seeing(kh, HALF_CLEAN, kblock0, L, S, kvalid);
     WalkPos cur = first;
+    uint32_t bcur = 0;  // byte offset of tile t's buffer (tile t + 1's follows, modulo NBUF)
     auto step = [&](int t, f32x16& sc, f32x16& dc, f32x16& sn, f32x16& dn) __attribute__((always_inline)) {
-      const int qh = cur.qh, i = cur.tile(wk);
+      const int qh = cur.qh, q0 = cur.tile(wk) * BM;
       cur.next(wk);
-      const int q0 = i * BM, q1 = imin(L, q0 + BM);
-      // (EMPTY tiles are never visited; the window test would mask all of one)
-      const int cls = classify_vs_key_tile(kh, kA, kB, S, qh, q0, q1, (q1 - q0) == BM && (k1 - k0) == BN);
-      const PosWindow win = queries_seeing(kh, qh, kblock0, L, S, kvalid);
-      const int rel = q0 + 4 * g2 - win.lo;
-      const unsigned span = (unsigned)(win.hi - win.lo);
-      const char* bt = sm.buf[t % Smem::NBUF];
-      const char* bn = sm.buf[(t + 1) % Smem::NBUF];
+      const uint32_t bnext = bcur == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcur + Smem::BUF;
+      const char* bt = sm.buf[0] + bcur;
+      const char* bn = sm.buf[0] + bnext;
+      bcur = bnext;
       char* xw = sm.x[t & 1];
-      if (cls == TILE_FULL) {
+      // (EMPTY tiles are never visited; the window test would mask all of one)
+      if (fr.full(qh, q0, BM)) {
         scores(bn, sn, dn);
-        softmax_grad(bt, xw, sc, dc, rel, span, Flag<false>());
+        softmax_grad(bt, xw, sc, dc, 0, 0u, Flag<false>());
       } else {
+        const PosWindow win = qh == HALF_NOISY ? win_n : win_c;
         scores(bn, sn, dn);
-        softmax_grad(bt, xw, sc, dc, rel, span, Flag<true>());
+        softmax_grad(bt, xw, sc, dc, q0 + 4 * g2 - win.lo, (unsigned)(win.hi - win.lo), Flag<true>());
       }
     };
     f32x16 sA, dA, sB, dB;
@@ -223,13 +227,19 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     constexpr int NC = 2 * decltype(copy)::NI + 1;  // vector-memory instructions per query-tile copy
     // Q, dO and (lse2, delta) of one query tile.  The four waves copy the
     // row pairs each (the same data), so every wave issues NC instructions.
+    // Addresses: the group's first query head is fixed, so a step adds one
+    // row offset (head g, packed row row0) to three base pointers.
+    const size_t g0row = ((size_t)b * p.Hq + (size_t)hk * p.G) * N;  // first row of the group's first head
+    const bf16* const qg = p.Q + g0row * D;
+    const bf16* const dog = p.dO + g0row * D;
+    const float* const rsg = p.rs + 2 * g0row;
     auto issue = [&](WalkPos wp, char* dst) {
-      const int qh = wp.qh, i = wp.tile(wk);
-      const size_t hrow = ((size_t)b * p.Hq + hk * p.G + wp.g) * N;  // first row of the head
-      const int row0 = qh * L + i * BM;
-      copy.issue(p.Q + hrow * D, N, row0, dst);
-      copy.issue(p.dO + hrow * D, N, row0, dst + Smem::DO_OFF);
-      async_load_row_floats(p.rs + 2 * hrow, 2 * N, 2 * row0, reinterpret_cast<float*>(dst + Smem::RS_OFF), lane);
+      const int row0 = wp.qh * L + wp.tile(wk) * BM;
+      const size_t r = (size_t)wp.g * N + row0;  // row within the group's heads
+      const int left = N - row0;                 // rows of this head from row0 on
+      copy.issue_rows(qg + r * D, left, dst);
+      copy.issue_rows(dog + r * D, left, dst + Smem::DO_OFF);
+      async_load_row_floats(rsg + 2 * r, 2 * left, 0, reinterpret_cast<float*>(dst + Smem::RS_OFF), lane);
     };
     // tiles 0, 1 and 2 (the last tile again past the end); cp then points at tile 3
     WalkPos cp = first;
@@ -282,8 +292,12 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
         issue(t + 3 < T ? cp : last, bn);
       }
     };
+    uint32_t bcons = (Smem::NBUF - 1) * Smem::BUF;  // buffer of tile t - 1
+    uint32_t bcopy = 3 * Smem::BUF;                  // buffer tile t + 3 is copied into
     for (int t = 0; t < steps; ++t) {
-      consume(sm.buf[(t + Smem::NBUF - 1) % Smem::NBUF], sm.x[(t + 1) & 1], sm.buf[(t + 3) % Smem::NBUF], t);
+      consume(sm.buf[0] + bcons, sm.x[(t + 1) & 1], sm.buf[0] + bcopy, t);
+      bcons = bcons == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcons + Smem::BUF;
+      bcopy = bcopy == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcopy + Smem::BUF;
       if (t + 3 < T) cp.next(wk);
       compute_fence();
       wait_global_loads_but<NC>();  // tile t + 2 has landed (the copy issued this step may not have)
@@ -422,8 +436,6 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
-  const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;
-
   const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
 
   const int r = q0 + w * 32 + l32;
@@ -435,11 +447,18 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
-  auto issue = [&](int t, char* kdst, char* vdst) {
+  const bf16* const kbase = p.K + kvbase;
+  const bf16* const vbase = p.V + kvbase;
+  // first packed row of key tile t (2L rows for this batch and KV head)
+  auto tile_row = [&](int t) {
     int kh, j;
     kl.at(t, kh, j);
-    copy.issue(p.K + kvbase, N, kh * L + j * BN, kdst);
-    copy.issue(p.V + kvbase, N, kh * L + j * BN, vdst);
+    return kh * L + j * BN;
+  };
+  auto issue = [&](int t, char* kdst, char* vdst) {
+    const int r = tile_row(t);
+    copy.issue_rows(kbase + (size_t)r * D, N - r, kdst);
+    copy.issue_rows(vbase + (size_t)r * D, N - r, vdst);
   };
   constexpr int DQ_COPIES = 2 * decltype(copy)::NI;
   if (T > 0) issue(0, lds, lds + 2 * TILE);
@@ -473,6 +492,12 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   wait_global_loads();
   __syncthreads();
 
+  // Per-step bookkeeping as in the forward kernel: a two-comparison FULL
+  // test and the visibility windows of both key halves computed once.
+  const FullRange fr = full_range_vs_query_tile(qh, q0, q1, L, S, BM);
+  const PosWindow win_n = keys_visible_from(qh, HALF_NOISY, qblock0, L, S, qvalid);
+  const PosWindow win_c = keys_visible_from(qh, HALF_CLEAN, qblock0, L, S, qvalid);
+
   // One key tile; restrict-qualified current and next buffers as in the
   // forward kernel, so the copy in flight does not make the compiler wait
   // before the reads of the current tile.  The copy of the next tile is
@@ -481,8 +506,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
                        char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
     int kh, j;
     kl.at(t, kh, j);
-    const int k0 = j * BN, k1 = imin(L, k0 + BN);
-    const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
+    const int k0 = j * BN;
+    const bool full = fr.full(kh, k0, BN);
     {
       f32x16 sacc[KB], dpacc[KB];
 #pragma unroll
@@ -493,10 +518,9 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
           dpacc[kb][e] = 0.f;
         }
       // the next tile's copy, one instruction per step of the loop below
-      int khn, jn;
-      kl.at(imin(t + 1, T - 1), khn, jn);
-      const __amdgpu_buffer_rsrc_t kn = decltype(copy)::rows(p.K + kvbase, N, khn * L + jn * BN);
-      const __amdgpu_buffer_rsrc_t vn = decltype(copy)::rows(p.V + kvbase, N, khn * L + jn * BN);
+      const int rn = tile_row(imin(t + 1, T - 1));
+      const __amdgpu_buffer_rsrc_t kn = make_buffer(kbase + (size_t)rn * D, (uint32_t)((N - rn) * D * 2));
+      const __amdgpu_buffer_rsrc_t vn = make_buffer(vbase + (size_t)rn * D, (uint32_t)((N - rn) * D * 2));
       // S^T[key][q] = sum_d K[key][d] Q[q][d];  dP^T[key][q] = sum_d V[key][d] dO[q][d]
 #pragma unroll
       for (int s = 0; s < DS; ++s) {
@@ -515,7 +539,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       }
       interleave_copies<2 * DS * KB, DQ_COPIES>();
       // dS = P (dP - delta); FULL tiles without the per-element visibility test
-      const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
+      const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
       const unsigned span = (unsigned)(win.hi - win.lo);
       const int rel = k0 + 4 * g2 - win.lo;
       auto ds = [&](auto masked) __attribute__((always_inline)) {
@@ -532,7 +556,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
             }
       };
       // (EMPTY is never visited; it would take the masked path, which masks all of it)
-      if (cls == TILE_FULL) ds(Flag<false>());
+      if (full) ds(Flag<false>());
       else ds(Flag<true>());
       bf16x8 dsb[PC];
 #pragma unroll

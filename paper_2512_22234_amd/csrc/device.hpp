@@ -183,6 +183,13 @@ struct TileCopy {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rsrc, (__attribute__((address_space(3))) void*)(dst + (u * NW + wave) * 1024), 16, (int)boff[u], 0, 0, 0);
   }
+  // Copy the NR rows starting at `first` (of which `left` lie inside the
+  // array; the rest read as zero) into the tile at dst.
+  __device__ void issue_rows(const bf16* first, int left, char* dst) const {
+    const __amdgpu_buffer_rsrc_t rsrc = make_buffer(first, (uint32_t)(left * D * 2));
+#pragma unroll
+    for (int u = 0; u < NI; ++u) issue_one(rsrc, dst, u);
+  }
   // Copy rows [row0, row0 + NR) of arr[nrows][D] into the tile at dst.
   __device__ void issue(const bf16* arr, int nrows, int row0, char* dst) const {
     const __amdgpu_buffer_rsrc_t rsrc = rows(arr, nrows, row0);

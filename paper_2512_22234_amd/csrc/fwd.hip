@@ -68,7 +68,6 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
-  const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;  // first rows of the tile's first and last block
 
   const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
 
@@ -80,11 +79,18 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
   const TileCopy<D, BN, 256> copy(tid);
-  // copy key tile t of K or V (2L rows each for this batch and KV head)
-  auto issue = [&](int t, bool is_v, char* dst) {
+  const bf16* const kbase = p.K + kvbase;
+  const bf16* const vbase = p.V + kvbase;
+  // first packed row of key tile t (2L rows for this batch and KV head)
+  auto tile_row = [&](int t) {
     int kh, j;
     kl.at(t, kh, j);
-    copy.issue((is_v ? p.V : p.K) + kvbase, N, kh * L + j * BN, dst);
+    return kh * L + j * BN;
+  };
+  // copy key tile t of K or V
+  auto issue = [&](int t, bool is_v, char* dst) {
+    const int r = tile_row(t);
+    copy.issue_rows((is_v ? vbase : kbase) + (size_t)r * D, N - r, dst);
   };
 
   if (T > 0) {
@@ -111,6 +117,13 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   wait_global_loads();
   __syncthreads();
 
+  // Per-step bookkeeping is a few scalar instructions: the FULL test is two
+  // comparisons against per-workgroup bounds and the visibility windows of
+  // both key halves are computed once.
+  const FullRange fr = full_range_vs_query_tile(qh, q0, q1, L, S, BM);
+  const PosWindow win_n = keys_visible_from(qh, HALF_NOISY, qblock0, L, S, qvalid);
+  const PosWindow win_c = keys_visible_from(qh, HALF_CLEAN, qblock0, L, S, qvalid);
+
   // One key tile.  The current K/V tiles and the buffers the next tile is
   // copied into are distinct restrict-qualified pointers: the alias scopes
   // this gives every LDS access let the compiler see that the copy in flight
@@ -128,10 +141,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
     const int tn = imin(t + 1, T - 1);
     int kh, j;
     kl.at(t, kh, j);
-    const int k0 = j * BN, k1 = imin(L, k0 + BN);
+    const int k0 = j * BN;
     // (EMPTY tiles are never visited; were one visited, the window test of
     // PARTIAL tiles would mask all of it)
-    const int cls = classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, (q1 - q0) == BM && (k1 - k0) == BN);
+    const bool full = fr.full(kh, k0, BN);
     {
       f32x16 sacc[KB];
 #pragma unroll
@@ -145,9 +158,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
         for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
       issue(tn, false, knxt);
       interleave_copies<DS * KB, decltype(copy)::NI>();
-      if (cls != TILE_FULL) {
+      if (!full) {
         // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
-        const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
+        const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
         const unsigned span = (unsigned)(win.hi - win.lo);
         const int rel = k0 + 4 * g2 - win.lo;
 #pragma unroll

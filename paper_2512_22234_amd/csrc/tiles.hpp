@@ -106,6 +106,54 @@ BD_HD int classify_vs_key_tile(int kh, int A, int B, int S, int qh, int q0, int 
   return cls;
 }
 
+// The FULL test of classify_vs_key_tile / classify_vs_query_tile for a
+// visited pair, reduced to two comparisons per step: with one tile fixed, a
+// moving tile [x0, x0 + n) of half h (n its full size) is FULL iff
+// lo(h) <= x0 and x0 + n <= hi(h); hi < 0 means never.  A FULL tile is
+// full-sized, so the moving tile's own size check is x0 + n <= L.
+struct FullRange {
+  int lo_n, hi_n, lo_c, hi_c;  // for a moving tile in the noisy / clean half
+  BD_HD bool full(int half, int x0, int n) const {
+    return half == HALF_NOISY ? (x0 >= lo_n && x0 + n <= hi_n) : (x0 >= lo_c && x0 + n <= hi_c);
+  }
+};
+// Fixed key tile [k0, k1) of half kh (full-sized iff k1 - k0 == BN); moving query tiles.
+BD_HD FullRange full_range_vs_key_tile(int kh, int k0, int k1, int L, int S, int BN) {
+  const int A = (k0 / S) * S, B = ((k1 - 1) / S) * S;
+  const bool kfull = (k1 - k0) == BN;
+  FullRange r;
+  if (kh == HALF_CLEAN) {
+    r.lo_n = B + S;  // noisy queries of later blocks only
+    r.hi_n = kfull ? L : -1;
+    r.lo_c = B;      // clean queries of the same or later blocks
+    r.hi_c = kfull ? L : -1;
+  } else {
+    r.lo_n = A;      // noisy queries of the key tile's own (single) block
+    r.hi_n = (kfull && A == B) ? imin(L, A + S) : -1;
+    r.lo_c = 0;
+    r.hi_c = -1;     // clean queries never see noisy keys
+  }
+  return r;
+}
+// Fixed query tile [q0, q1) of half qh (full-sized iff q1 - q0 == BM); moving key tiles.
+BD_HD FullRange full_range_vs_query_tile(int qh, int q0, int q1, int L, int S, int BM) {
+  const int A = (q0 / S) * S, B = ((q1 - 1) / S) * S;
+  const bool qfull = (q1 - q0) == BM;
+  FullRange r;
+  if (qh == HALF_NOISY) {
+    r.lo_n = A;      // noisy keys of the query tile's own (single) block
+    r.hi_n = (qfull && A == B) ? imin(L, A + S) : -1;
+    r.lo_c = 0;      // clean keys of strictly earlier blocks
+    r.hi_c = qfull ? A : -1;
+  } else {
+    r.lo_n = 0;
+    r.hi_n = -1;     // clean queries never see noisy keys
+    r.lo_c = 0;      // clean keys of the same or earlier blocks
+    r.hi_c = qfull ? imin(L, A + S) : -1;
+  }
+  return r;
+}
+
 // Visible positions of the other half for one row, as a half-open window of
 // local positions [lo, hi) (empty when lo == hi).  pos_block_start = b*S for
 // the row's block b.  Past-the-end rows pass valid = false.
