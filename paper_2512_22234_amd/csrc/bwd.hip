@@ -537,7 +537,9 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
           else if (u < 2 * NI) copy.issue_one(vn, vnxt, u - NI);
         }
       }
-      interleave_copies<2 * DS * KB, DQ_COPIES>();
+      // operand reads four MFMAs ahead (a read's latency exceeds one MFMA),
+      // the copy spread between the MFMAs
+      pipeline_reads_and_copies<2 * DS * KB, 4, 1, DQ_COPIES>();
       // dS = P (dP - delta); FULL tiles without the per-element visibility test
       const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
       const unsigned span = (unsigned)(win.hi - win.lo);

@@ -220,6 +220,23 @@ __device__ inline void interleave_copies() {
   }
 }
 
+// Scheduling request for the current basic block of NM MFMAs that each take
+// RPM LDS operand reads and share NV copy instructions: the reads run AHEAD
+// MFMAs ahead of their use and the copies are spread evenly between the
+// MFMAs.  Place it after the block's last instruction.
+template <int NM, int AHEAD, int RPM, int NV>
+__device__ inline void pipeline_reads_and_copies() {
+  static_assert(AHEAD >= 1 && AHEAD <= NM && (NV == 0 || NM >= NV), "schedule shape");
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD * RPM, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    if (i + AHEAD < NM) __builtin_amdgcn_sched_group_barrier(0x100, RPM, 0);
+    if (NV > 0 && i % (NM / (NV > 0 ? NV : 1)) == 0 && i / (NM / (NV > 0 ? NV : 1)) < NV)
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (tile copy)
+  }
+}
+
 // Scheduling request for the current basic block: LDS operand reads run
 // AHEAD MFMAs ahead of their use.  The first AHEAD * RPM reads (plus FIRST
 // more, e.g. operands shared by all MFMAs) go first, then each MFMA is

@@ -157,7 +157,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
       issue(tn, false, knxt);
-      interleave_copies<DS * KB, decltype(copy)::NI>();
+      // K operand reads four MFMAs ahead, the copy spread between the MFMAs
+      pipeline_reads_and_copies<DS * KB, 4, 1, decltype(copy)::NI>();
       if (!full) {
         // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
         const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
