@@ -12,4 +12,7 @@ from .bd_attn_oracle import (  # noqa: F401
     backward,
     probabilities,
     sampled,
+    varlen_visibility_mask,
+    varlen_forward,
+    varlen_backward,
 )

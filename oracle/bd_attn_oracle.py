@@ -226,3 +226,91 @@ def sampled(dO, Q, K, V, L: int, S: int, b: int, hkv: int, query_rows, key_rows,
                     out["dK"] += scale * (dS[:, kr].T @ Qb[h, idx])
                     out["dV"] += P[:, kr].T @ dOc
     return out
+
+
+# ---------------------------------------------------------------------------
+# Several sequences packed into one buffer (the dynamic packing that
+# Section 5.2 names as the next speed-up of blockwise training).
+#
+# Sequence i of length L_i (tokens per copy) occupies packed rows
+# [2 c_i, 2 c_{i+1}) of every head, c = cumulative lengths (c_0 = 0): its noisy
+# copy x_t first, then its clean copy x_0, exactly the single-sequence layout
+# of Section 4.1.  A query sees a key iff both lie in the same sequence and
+# that sequence's mask (Eq. 1 / Eq. 2 at their local positions) allows the
+# pair.  Sequences never see each other; a sequence of length 0 has no rows.
+
+def varlen_visibility_mask(lengths, S: int) -> np.ndarray:
+    """Boolean [2T, 2T] mask of the packed layout, T = sum(lengths), built
+    from the per-pair rule: same sequence, then noisy query -> noisy key of
+    the same block or clean key of an earlier block; clean query -> clean key
+    of the same or an earlier block; clean query -> noisy key never."""
+    lengths = [int(x) for x in lengths]
+    if S < 1 or any(x < 0 for x in lengths):
+        raise ValueError("S >= 1 and lengths >= 0 required")
+    seq, local, Ls = [], [], []
+    for i, Li in enumerate(lengths):
+        seq += [i] * (2 * Li)
+        local += list(range(2 * Li))
+        Ls += [Li] * (2 * Li)
+    seq, local, Ls = np.array(seq, dtype=np.int64), np.array(local, dtype=np.int64), np.array(Ls, dtype=np.int64)
+    if seq.size == 0:
+        return np.zeros((0, 0), dtype=bool)
+    noisy = local < Ls
+    b = np.where(Ls > 0, (local % np.maximum(Ls, 1)) // S, 0)
+    same = seq[:, None] == seq[None, :]
+    nq, nk = noisy[:, None], noisy[None, :]
+    bq, bk = b[:, None], b[None, :]
+    M = same & ((nq & nk & (bq == bk)) | (nq & ~nk & (bk < bq)) | (~nq & ~nk & (bk <= bq)))
+    assert M.any(axis=1).all()
+    return M
+
+
+def _check_varlen(Q, K, V, lengths):
+    if Q.ndim != 3 or K.ndim != 3 or V.shape != K.shape:
+        raise ValueError("Q [Hq,2T,D], K/V [Hkv,2T,D] expected")
+    Hq, N, D = Q.shape
+    Hkv = K.shape[0]
+    if N != 2 * sum(lengths) or K.shape[1] != N or K.shape[2] != D or Hq % Hkv:
+        raise ValueError("inconsistent shapes")
+    return Hq, Hkv, D
+
+
+def varlen_forward(Q, K, V, lengths, S: int, scale: float | None = None):
+    """O [Hq,2T,D] and LSE [Hq,2T] of the packed sequences: dense masked
+    softmax attention over all 2T packed rows with varlen_visibility_mask."""
+    Q, K, V = _as64(Q), _as64(K), _as64(V)
+    Hq, Hkv, D = _check_varlen(Q, K, V, lengths)
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = varlen_visibility_mask(lengths, S)
+    O = np.zeros(Q.shape)
+    LSE = np.zeros(Q.shape[:2])
+    for h in range(Hq):
+        P, m, l = _softmax_rows(scale * (Q[h] @ K[h // G].T), M)
+        O[h] = P @ V[h // G]
+        LSE[h] = (m + np.log(l))[:, 0]
+    return O, LSE
+
+
+def varlen_backward(dO, Q, K, V, lengths, S: int, scale: float | None = None):
+    """dQ, dK, dV of <dO, O> for the packed sequences (the same textbook
+    vector-Jacobian product as backward, over the packed mask)."""
+    dO, Q, K, V = _as64(dO), _as64(Q), _as64(K), _as64(V)
+    Hq, Hkv, D = _check_varlen(Q, K, V, lengths)
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    M = varlen_visibility_mask(lengths, S)
+    dQ = np.zeros(Q.shape)
+    dK = np.zeros(K.shape)
+    dV = np.zeros(V.shape)
+    for h in range(Hq):
+        g = h // G
+        P, _, _ = _softmax_rows(scale * (Q[h] @ K[g].T), M)
+        O = P @ V[g]
+        dP = dO[h] @ V[g].T
+        delta = (dO[h] * O).sum(axis=1, keepdims=True)
+        dS = P * (dP - delta)
+        dQ[h] = scale * (dS @ K[g])
+        dK[g] += scale * (dS.T @ Q[h])
+        dV[g] += P.T @ dO[h]
+    return dQ, dK, dV

@@ -10,7 +10,11 @@
   and torch-autograd gradients;
 * finite differences of <dO, O>;
 * invariants: clean-half independence, GQA = repeated-KV MHA, equivariance
-  under permutations inside a noisy block, softmax rows summing to one.
+  under permutations inside a noisy block, softmax rows summing to one;
+* packed sequences (varlen): the packed mask against plain pair-by-pair loops,
+  one sequence against the single-sequence mask, equal lengths against the
+  batched oracle, each sequence against its own batched call, independence of
+  the sequences, and finite differences.
 """
 import math
 import os
@@ -330,3 +334,116 @@ def test_sampled_matches_full_evaluation():
     np.testing.assert_allclose(s["dQ"], dQ[1, 2:4][:, qr], atol=1e-12, rtol=0)
     np.testing.assert_allclose(s["dK"], dK[1, 1, kr], atol=1e-12, rtol=0)
     np.testing.assert_allclose(s["dV"], dV[1, 1, kr], atol=1e-12, rtol=0)
+
+
+# ------------------------------------------------- packed sequences (varlen)
+
+def _varlen_mask_by_loops(lengths, S):
+    """The packed mask pair by pair with plain loops: locate each row's
+    sequence and local position by walking the lengths, then apply the
+    single-sequence rule of Eq. 1 / Eq. 2 when both rows share a sequence."""
+    rows = []
+    for i, Li in enumerate(lengths):
+        for local in range(2 * Li):
+            rows.append((i, local, Li))
+    N = len(rows)
+    M = np.zeros((N, N), dtype=bool)
+    for q, (iq, pq, Lq) in enumerate(rows):
+        for k, (ik, pk, Lk) in enumerate(rows):
+            if iq != ik:
+                continue
+            q_noisy, k_noisy = pq < Lq, pk < Lk
+            bq, bk = (pq % Lq) // S, (pk % Lk) // S
+            if q_noisy and k_noisy:
+                M[q, k] = bq == bk
+            elif q_noisy:
+                M[q, k] = bk < bq
+            elif not k_noisy:
+                M[q, k] = bk <= bq
+    return M
+
+
+@pytest.mark.parametrize("lengths", [[1], [3], [2, 3], [4, 0, 1], [5, 2, 3], [0, 7, 0], [6, 6]])
+def test_varlen_mask_brute_force(lengths):
+    for S in range(1, 8):
+        np.testing.assert_array_equal(oracle.varlen_visibility_mask(lengths, S), _varlen_mask_by_loops(lengths, S),
+                                      err_msg=f"S={S}")
+
+
+def test_varlen_mask_one_sequence_is_the_single_mask():
+    for L in (1, 5, 8, 13):
+        for S in (1, 2, 3, 8, 20):
+            np.testing.assert_array_equal(oracle.varlen_visibility_mask([L], S), oracle.visibility_mask(L, S))
+
+
+def _pack(x):
+    """[B, H, 2L, D] -> [H, 2BL, D]: sequence b at packed rows [2bL, 2(b+1)L)."""
+    B, H, N, D = x.shape
+    return np.transpose(x, (1, 0, 2, 3)).reshape(H, B * N, D)
+
+
+def test_varlen_equal_lengths_match_batched_forward_backward():
+    B, Hq, Hkv, L, S, D = 3, 4, 2, 9, 2, 8
+    Q, K, V, dO = (_rand(s, i) for i, s in enumerate([(B, Hq, 2 * L, D), (B, Hkv, 2 * L, D),
+                                                      (B, Hkv, 2 * L, D), (B, Hq, 2 * L, D)]))
+    O, LSE = oracle.forward(Q, K, V, L, S)
+    dQ, dK, dV = oracle.backward(dO, Q, K, V, L, S)
+    Ov, LSEv = oracle.varlen_forward(_pack(Q), _pack(K), _pack(V), [L] * B, S)
+    dQv, dKv, dVv = oracle.varlen_backward(_pack(dO), _pack(Q), _pack(K), _pack(V), [L] * B, S)
+    np.testing.assert_allclose(Ov, _pack(O), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(LSEv, np.transpose(LSE, (1, 0, 2)).reshape(Hq, -1), rtol=1e-12, atol=1e-12)
+    for a, b in ((dQv, dQ), (dKv, dK), (dVv, dV)):
+        np.testing.assert_allclose(a, _pack(b), rtol=1e-10, atol=1e-12)
+
+
+def test_varlen_each_sequence_matches_its_own_batched_call():
+    lengths, S, Hq, Hkv, D = [5, 0, 11, 1, 7], 3, 4, 1, 8
+    T = sum(lengths)
+    Q, K, V, dO = (_rand(s, 10 + i) for i, s in enumerate([(Hq, 2 * T, D), (Hkv, 2 * T, D),
+                                                           (Hkv, 2 * T, D), (Hq, 2 * T, D)]))
+    O, LSE = oracle.varlen_forward(Q, K, V, lengths, S)
+    dQ, dK, dV = oracle.varlen_backward(dO, Q, K, V, lengths, S)
+    c = 0
+    for Li in lengths:
+        if Li:
+            r = slice(2 * c, 2 * (c + Li))
+            Oi, LSEi = oracle.forward(Q[None, :, r], K[None, :, r], V[None, :, r], Li, S)
+            dQi, dKi, dVi = oracle.backward(dO[None, :, r], Q[None, :, r], K[None, :, r], V[None, :, r], Li, S)
+            np.testing.assert_allclose(O[:, r], Oi[0], rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(LSE[:, r], LSEi[0], rtol=1e-12, atol=1e-12)
+            for a, b in ((dQ[:, r], dQi[0]), (dK[:, r], dKi[0]), (dV[:, r], dVi[0])):
+                np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-12)
+        c += Li
+
+
+def test_varlen_sequences_do_not_see_each_other():
+    lengths, S, D = [6, 4], 2, 4
+    T = sum(lengths)
+    Q, K, V = (_rand((2, 2 * T, D), 30 + i) for i in range(3))
+    O, _ = oracle.varlen_forward(Q, K, V, lengths, S)
+    K2, V2 = K.copy(), V.copy()
+    K2[:, 12:] += 3.0  # the second sequence's rows
+    V2[:, 12:] -= 2.0
+    O2, _ = oracle.varlen_forward(Q, K2, V2, lengths, S)
+    np.testing.assert_array_equal(O[:, :12], O2[:, :12])
+    assert not np.allclose(O[:, 12:], O2[:, 12:])
+
+
+def test_varlen_backward_finite_differences():
+    lengths, S, D = [3, 2], 2, 3
+    T = sum(lengths)
+    Q, K, V, dO = _rand((2, 2 * T, D), 40), _rand((1, 2 * T, D), 41), _rand((1, 2 * T, D), 42), _rand((2, 2 * T, D), 43)
+    dQ, dK, dV = oracle.varlen_backward(dO, Q, K, V, lengths, S)
+    f = lambda q, k, v: float((dO * oracle.varlen_forward(q, k, v, lengths, S)[0]).sum())
+    h = 1e-6
+    for X, G in ((Q, dQ), (K, dK), (V, dV)):
+        for idx in [(0, 0, 0), (0, 3, 2), (0, 7, 1), (0, 9, 0)]:
+            if X.shape[0] <= idx[0]:
+                continue
+            Xp, Xm = X.copy(), X.copy()
+            Xp[idx] += h
+            Xm[idx] -= h
+            args_p = [Xp if Y is X else Y for Y in (Q, K, V)]
+            args_m = [Xm if Y is X else Y for Y in (Q, K, V)]
+            fd = (f(*args_p) - f(*args_m)) / (2 * h)
+            assert abs(fd - G[idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, G[idx])
