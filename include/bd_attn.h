@@ -147,6 +147,41 @@ int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void*
                        void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream,
                        hipEvent_t* marks, int n_marks);
 
+/*
+ * Packed sequences ("dynamic packing", named in Section 5.2 as the next
+ * speed-up of blockwise training): n_seqs sequences of different lengths in
+ * one buffer, each a [x_t | x_0] pair with the mask of Section 4.1 (Eq. 1 and
+ * Eq. 2 at the sequence's own positions); sequences never attend to each
+ * other.
+ *
+ * cu_seqlens: DEVICE array of n_seqs + 1 int32 values (4-byte aligned),
+ *   cu_seqlens[0] = 0, non-decreasing, cu_seqlens[n_seqs] = total_L; sequence
+ *   i has L_i = cu_seqlens[i+1] - cu_seqlens[i] tokens per copy (0 allowed).
+ *   It is read by the kernels only, not by the host.
+ * max_L: an upper bound on every L_i (it sizes the launch grids); 1 <= max_L
+ *   <= 2^22.  A sequence longer than max_L is only partly computed: the caller
+ *   must pass a true bound.
+ * Layouts (contiguous, innermost last): Q, O, dO, dQ [Hq, 2*total_L, D];
+ *   K, V, dK, dV [Hkv, 2*total_L, D]; LSE [Hq, 2*total_L].  Sequence i occupies
+ *   rows [2*cu_seqlens[i], 2*cu_seqlens[i+1]) of every head: its noisy copy,
+ *   then its clean copy.
+ * S: block size, the same for every sequence (a sequence shorter than S is
+ *   one block).  Everything else (dtype, scale, workspace, ownership, stream
+ *   order, errors, determinism) is as for bd_attn_fwd / bd_attn_bwd; with
+ *   total_L = 0 the calls validate and enqueue nothing.
+ */
+int bd_attn_varlen_fwd(const void* Q, const void* K, const void* V, const int32_t* cu_seqlens, int n_seqs,
+                       int total_L, int max_L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                       void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream);
+int bd_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                       const float* LSE, const int32_t* cu_seqlens, int n_seqs, int total_L, int max_L,
+                       int S, int Hq, int Hkv, int D, float scale, int dtype,
+                       void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Workspace bytes for bd_attn_varlen_fwd (for_bwd = 0) or bd_attn_varlen_bwd
+ * (for_bwd = 1); 0 for arguments the calls would reject. */
+size_t bd_attn_varlen_workspace_bytes(int n_seqs, int total_L, int max_L, int S, int Hq, int Hkv, int D,
+                                      int dtype, int for_bwd);
+
 /* Comma-separated names of the kernels bd_attn_fwd (for_bwd = 0) or
  * bd_attn_bwd (for_bwd = 1) launch for `dtype`, in launch order (static). */
 const char* bd_attn_stage_names(int for_bwd, int dtype);

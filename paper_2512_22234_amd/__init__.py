@@ -28,6 +28,8 @@ __all__ = [
     "bd_attn_status_string",
     "bd_attn_version", "bd_attn_fwd_marked", "bd_attn_bwd_marked", "bd_attn_stage_names",
     "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
+    "bd_attn_varlen", "BdAttnVarlenFunction", "bd_attn_varlen_fwd", "bd_attn_varlen_bwd",
+    "bd_attn_varlen_workspace_bytes",
 ]
 
 
@@ -216,3 +218,99 @@ class BdAttnFunction(torch.autograd.Function):
 def bd_attn(q, k, v, L: int, S: int, scale=None):
     """Block-diffusion masked attention over [x_t | x_0]; differentiable."""
     return BdAttnFunction.apply(q, k, v, L, S, scale)
+
+
+# ---------------------------------------------------------------------------
+# Packed sequences: q [Hq, 2T, D], k/v [Hkv, 2T, D], cu_seqlens int32 [n+1] on
+# the same device (cu_seqlens[0] = 0, cu_seqlens[n] = T); sequence i occupies
+# rows [2 cu[i], 2 cu[i+1]) of every head, noisy copy first.
+
+def bd_attn_varlen_workspace_bytes(n_seqs, total_L, max_L, S, Hq, Hkv, D, dtype, for_bwd) -> int:
+    return int(lib().bd_attn_varlen_workspace_bytes(n_seqs, total_L, max_L, S, Hq, Hkv, D, int(dtype),
+                                                      int(for_bwd)))
+
+
+def _varlen_shapes(q, k, cu_seqlens):
+    if q.dim() != 3 or k.dim() != 3:
+        raise ValueError("q [Hq,2T,D] and k/v [Hkv,2T,D] expected")
+    Hq, N, D = q.shape
+    Hkv = k.shape[0]
+    if N % 2:
+        raise ValueError(f"packed length {N} is odd")
+    if cu_seqlens.dtype != torch.int32 or cu_seqlens.dim() != 1 or cu_seqlens.numel() < 2:
+        raise ValueError("cu_seqlens must be a 1-D int32 tensor of n_seqs + 1 entries")
+    if cu_seqlens.device != q.device or not cu_seqlens.is_contiguous():
+        raise ValueError("cu_seqlens must be contiguous and on q's device")
+    return Hq, Hkv, D, N // 2, cu_seqlens.numel() - 1
+
+
+def bd_attn_varlen_fwd(q, k, v, cu_seqlens, max_L: int, S: int, scale=None, out=None, lse=None,
+                       workspace=None, stream=None):
+    """Forward pass over packed sequences; returns (O, LSE [Hq, 2T] float32)."""
+    Hq, Hkv, D, T, n = _varlen_shapes(q, k, cu_seqlens)
+    dev, dt = q.device, q.dtype
+    code = _dtype_code(q)
+    _check("k", k, (Hkv, 2 * T, D), dt, dev)
+    _check("v", v, (Hkv, 2 * T, D), dt, dev)
+    o = torch.empty_like(q) if out is None else out
+    l_ = torch.empty((Hq, 2 * T), dtype=torch.float32, device=dev) if lse is None else lse
+    _check("out", o, q.shape, dt, dev)
+    _check("lse", l_, (Hq, 2 * T), torch.float32, dev)
+    nbytes = bd_attn_varlen_workspace_bytes(n, T, max_L, S, Hq, Hkv, D, code, 0)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    st = lib().bd_attn_varlen_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), n, T, max_L, S, Hq, Hkv, D,
+                                  _scale_arg(scale), code, _ptr(o), _ptr(l_), _ptr(ws), ws.numel(), sh)
+    if st:
+        raise BdAttnError(st, "bd_attn_varlen_fwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return o, l_
+
+
+def bd_attn_varlen_bwd(do, q, k, v, o, lse, cu_seqlens, max_L: int, S: int, scale=None, dq=None, dk=None,
+                       dv=None, workspace=None, stream=None):
+    """Backward pass over packed sequences; returns (dQ, dK, dV) in q's dtype."""
+    Hq, Hkv, D, T, n = _varlen_shapes(q, k, cu_seqlens)
+    dev, dt = q.device, q.dtype
+    code = _dtype_code(q)
+    for name, t, shp in (("do", do, q.shape), ("k", k, (Hkv, 2 * T, D)), ("v", v, (Hkv, 2 * T, D)),
+                         ("o", o, q.shape)):
+        _check(name, t, shp, dt, dev)
+    _check("lse", lse, (Hq, 2 * T), torch.float32, dev)
+    dq_ = torch.empty_like(q) if dq is None else dq
+    dk_ = torch.empty_like(k) if dk is None else dk
+    dv_ = torch.empty_like(v) if dv is None else dv
+    nbytes = bd_attn_varlen_workspace_bytes(n, T, max_L, S, Hq, Hkv, D, code, 1)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    st = lib().bd_attn_varlen_bwd(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(cu_seqlens), n,
+                                  T, max_L, S, Hq, Hkv, D, _scale_arg(scale), code, _ptr(dq_), _ptr(dk_),
+                                  _ptr(dv_), _ptr(ws), ws.numel(), sh)
+    if st:
+        raise BdAttnError(st, "bd_attn_varlen_bwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return dq_, dk_, dv_
+
+
+class BdAttnVarlenFunction(torch.autograd.Function):
+    """Autograd wrapper of the packed-sequence calls."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, cu_seqlens, max_L, S, scale=None):
+        o, lse = bd_attn_varlen_fwd(q, k, v, cu_seqlens, max_L, S, scale)
+        ctx.save_for_backward(q, k, v, o, lse, cu_seqlens)
+        ctx.max_L, ctx.S, ctx.scale = max_L, S, scale
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        q, k, v, o, lse, cu = ctx.saved_tensors
+        dq, dk, dv = bd_attn_varlen_bwd(do.contiguous(), q, k, v, o, lse, cu, ctx.max_L, ctx.S, ctx.scale)
+        return dq, dk, dv, None, None, None, None
+
+
+def bd_attn_varlen(q, k, v, cu_seqlens, max_L: int, S: int, scale=None):
+    """Block-diffusion masked attention over packed [x_t | x_0] sequences; differentiable."""
+    return BdAttnVarlenFunction.apply(q, k, v, cu_seqlens, max_L, S, scale)

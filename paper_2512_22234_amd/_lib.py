@@ -40,6 +40,13 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_fwd_marked.argtypes = L.bd_attn_fwd.argtypes + [vp, ci]
     L.bd_attn_bwd_marked.restype = ci
     L.bd_attn_bwd_marked.argtypes = L.bd_attn_bwd.argtypes + [vp, ci]
+    L.bd_attn_varlen_fwd.restype = ci
+    L.bd_attn_varlen_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, ci, vp, vp, vp, sz, vp]
+    L.bd_attn_varlen_bwd.restype = ci
+    L.bd_attn_varlen_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, ci,
+                                     vp, vp, vp, vp, sz, vp]
+    L.bd_attn_varlen_workspace_bytes.restype = sz
+    L.bd_attn_varlen_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ci]
     L.bd_attn_stage_names.restype = ctypes.c_char_p
     L.bd_attn_stage_names.argtypes = [ci, ci]
     L.bd_attn_workspace_bytes.restype = sz

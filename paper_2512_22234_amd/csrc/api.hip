@@ -26,18 +26,21 @@ bool shape_ok(int B, int L, int S, int Hq, int Hkv) {
   return B >= 1 && L >= 1 && S >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 && L <= (1 << 22);
 }
 
-Layout make_layout(int B, int L, int Hq, int Hkv, int D, int dtype, bool bwd) {
+// Rows of the Q-like and K-like arrays (per layout), times D elements each.
+size_t q_rows(const bd::Shape& s) { return s.seq.cu ? (size_t)s.Hq * 2 * s.seq.T : (size_t)s.B * s.Hq * 2 * s.L; }
+size_t k_rows(const bd::Shape& s) { return s.seq.cu ? (size_t)s.Hkv * 2 * s.seq.T : (size_t)s.B * s.Hkv * 2 * s.L; }
+
+Layout make_layout(const bd::Shape& s, int dtype, bool bwd) {
   Layout w;
-  const size_t N = 2 * (size_t)L;
-  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  const size_t nq = q_rows(s) * s.D, nk = k_rows(s) * s.D;
   size_t off = 0;
   if (bwd) {
     w.rs = off;
-    off += align256((size_t)B * Hq * N * 8);
+    off += align256(q_rows(s) * 8);
     w.part = off;
-    off += align256(bd::dkdv_partial_floats(B, Hkv, L, D) * 4);
+    off += align256(bd::dkdv_partial_floats(s) * 4);
     w.pair = off;
-    off += align256(bd::dkdv_pair_ints(B, Hkv, L) * 4);
+    off += align256(bd::dkdv_pair_ints(s.B, s.Hkv, s.L) * 4);
   }
   if (dtype == BD_ATTN_FP32) {
     w.q = off; off += align256(nq * 2);
@@ -67,7 +70,7 @@ bool overlap(const Range& a, const Range& b) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Common validation; fills the resolved shape.
+// Common validation; fills the resolved shape (fixed-length layout).
 int validate(int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, bd::Shape& s) {
   if (!shape_ok(B, L, S, Hq, Hkv)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
@@ -81,6 +84,34 @@ int validate(int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype
   s.D = D;
   s.G = Hq / Hkv;
   s.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)D);
+  s.seq = bd::SeqLayout{nullptr, 0};
+  return BD_ATTN_OK;
+}
+
+// Validation of the packed layout: n_seqs sequences, total_L tokens per copy
+// in all, none longer than max_L.  The lengths themselves live in device
+// memory (cu_seqlens) and are not read here.
+int validate_varlen(const int32_t* cu, int n_seqs, int total_L, int max_L, int S, int Hq, int Hkv, int D,
+                    float scale, int dtype, bd::Shape& s) {
+  if (n_seqs < 1 || total_L < 0 || max_L < 1 || max_L > (1 << 22) || S < 1 || Hq < 1 || Hkv < 1 ||
+      Hq % Hkv != 0)
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  // the pairing counters of the dK/dV kernel are indexed with 32-bit integers
+  if ((size_t)8 * n_seqs * Hkv * bd::cdiv(max_L, bd::DKV_BN) > (size_t)INT32_MAX) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (total_L > INT32_MAX / 2) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (cu == nullptr || !aligned(cu, 4)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (D != 64 && D != 128) return BD_ATTN_ERR_UNSUPPORTED;
+  if (dtype != BD_ATTN_BF16 && dtype != BD_ATTN_FP32) return BD_ATTN_ERR_UNSUPPORTED;
+  s.B = n_seqs;
+  s.L = max_L;
+  s.S = S > max_L ? max_L : S;  // a sequence shorter than S is one block either way
+  s.Hq = Hq;
+  s.Hkv = Hkv;
+  s.D = D;
+  s.G = Hq / Hkv;
+  s.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)D);
+  s.seq = bd::SeqLayout{cu, total_L};
   return BD_ATTN_OK;
 }
 
@@ -106,12 +137,12 @@ struct Marks {
   }
 };
 
-int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
-             float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream,
-             Marks marks);
-int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
-             int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
-             void* dV, void* ws, size_t ws_bytes, hipStream_t stream, Marks marks);
+// Work of one call on a validated shape.
+int fwd_impl(const bd::Shape& s, const void* Q, const void* K, const void* V, int dtype, void* O, float* LSE,
+             void* ws, size_t ws_bytes, hipStream_t stream, Marks marks);
+int bwd_impl(const bd::Shape& s, const void* dO, const void* Q, const void* K, const void* V, const void* O,
+             const float* LSE, int dtype, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
+             hipStream_t stream, Marks marks);
 
 }  // namespace
 
@@ -133,7 +164,15 @@ const char* bd_attn_status_string(int status) {
 size_t bd_attn_workspace_bytes(int B, int L, int S, int Hq, int Hkv, int D, int dtype, int for_bwd) {
   bd::Shape s;
   if (validate(B, L, S, Hq, Hkv, D, 0.f, dtype, s) != BD_ATTN_OK) return 0;
-  return make_layout(B, L, Hq, Hkv, D, dtype, for_bwd != 0).total;
+  return make_layout(s, dtype, for_bwd != 0).total;
+}
+
+size_t bd_attn_varlen_workspace_bytes(int n_seqs, int total_L, int max_L, int S, int Hq, int Hkv, int D, int dtype,
+                                      int for_bwd) {
+  bd::Shape s;
+  static const int32_t probe = 0;  // stands in for cu_seqlens: only the sizes matter here
+  if (validate_varlen(&probe, n_seqs, total_L, max_L, S, Hq, Hkv, D, 0.f, dtype, s) != BD_ATTN_OK) return 0;
+  return make_layout(s, dtype, for_bwd != 0).total;
 }
 
 int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out) {
@@ -231,29 +270,57 @@ int bd_attn_mask_windows_host(int L, int S, int by_key, int8_t* out) {
 
 int bd_attn_fwd(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
                 float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return fwd_impl(Q, K, V, B, L, S, Hq, Hkv, D, scale, dtype, O, LSE, ws, ws_bytes, stream, Marks{nullptr, 0});
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return fwd_impl(s, Q, K, V, dtype, O, LSE, ws, ws_bytes, stream, Marks{nullptr, 0});
 }
 
 int bd_attn_fwd_marked(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv,
                        int D, float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes,
                        hipStream_t stream, hipEvent_t* marks, int n_marks) {
-  return fwd_impl(Q, K, V, B, L, S, Hq, Hkv, D, scale, dtype, O, LSE, ws, ws_bytes, stream,
-                  Marks{marks, n_marks});
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return fwd_impl(s, Q, K, V, dtype, O, LSE, ws, ws_bytes, stream, Marks{marks, n_marks});
 }
 
 int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
                 int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
                 void* dV, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return bwd_impl(dO, Q, K, V, O, LSE, B, L, S, Hq, Hkv, D, scale, dtype, dQ, dK, dV, ws, ws_bytes, stream,
-                  Marks{nullptr, 0});
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, ws_bytes, stream, Marks{nullptr, 0});
 }
 
 int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void* V, const void* O,
                        const float* LSE, int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
                        void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream,
                        hipEvent_t* marks, int n_marks) {
-  return bwd_impl(dO, Q, K, V, O, LSE, B, L, S, Hq, Hkv, D, scale, dtype, dQ, dK, dV, ws, ws_bytes, stream,
-                  Marks{marks, n_marks});
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, ws_bytes, stream, Marks{marks, n_marks});
+}
+
+int bd_attn_varlen_fwd(const void* Q, const void* K, const void* V, const int32_t* cu_seqlens, int n_seqs,
+                       int total_L, int max_L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* O,
+                       float* LSE, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd::Shape s;
+  const int st = validate_varlen(cu_seqlens, n_seqs, total_L, max_L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return fwd_impl(s, Q, K, V, dtype, O, LSE, ws, ws_bytes, stream, Marks{nullptr, 0});
+}
+
+int bd_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                       const float* LSE, const int32_t* cu_seqlens, int n_seqs, int total_L, int max_L, int S,
+                       int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK, void* dV, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  bd::Shape s;
+  const int st = validate_varlen(cu_seqlens, n_seqs, total_L, max_L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, ws_bytes, stream, Marks{nullptr, 0});
 }
 
 const char* bd_attn_stage_names(int for_bwd, int dtype) {
@@ -267,23 +334,19 @@ const char* bd_attn_stage_names(int for_bwd, int dtype) {
 
 namespace {
 
-int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
-             float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream,
-             Marks marks) {
-  bd::Shape s;
-  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
-  if (st != BD_ATTN_OK) return st;
-  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, false);
+int fwd_impl(const bd::Shape& s, const void* Q, const void* K, const void* V, int dtype, void* O, float* LSE,
+             void* ws, size_t ws_bytes, hipStream_t stream, Marks marks) {
+  const Layout w = make_layout(s, dtype, false);
+  if (q_rows(s) == 0) return BD_ATTN_OK;  // packed layout with no tokens: nothing to read or write
   if (!Q || !K || !V || !O || !LSE || (w.total > 0 && !ws)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(LSE, 4) ||
       !aligned(ws, 16))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
-  const size_t N = 2 * (size_t)L;
-  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  const size_t nq = q_rows(s) * s.D, nk = k_rows(s) * s.D;
   const Range in[] = {{Q, nq * esz}, {K, nk * esz}, {V, nk * esz}};
-  const Range out[] = {{O, nq * esz}, {LSE, (size_t)B * Hq * N * 4}, {ws, w.total}};
+  const Range out[] = {{O, nq * esz}, {LSE, q_rows(s) * 4}, {ws, w.total}};
   for (const Range& o : out)
     for (const Range& i : in)
       if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
@@ -309,13 +372,11 @@ int fwd_impl(const void* Q, const void* K, const void* V, int B, int L, int S, i
   return BD_ATTN_OK;
 }
 
-int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const void* O, const float* LSE,
-             int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, void* dQ, void* dK,
-             void* dV, void* ws, size_t ws_bytes, hipStream_t stream, Marks marks) {
-  bd::Shape s;
-  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
-  if (st != BD_ATTN_OK) return st;
-  const Layout w = make_layout(B, L, Hq, Hkv, D, dtype, true);
+int bwd_impl(const bd::Shape& s, const void* dO, const void* Q, const void* K, const void* V, const void* O,
+             const float* LSE, int dtype, void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes,
+             hipStream_t stream, Marks marks) {
+  const Layout w = make_layout(s, dtype, true);
+  if (q_rows(s) == 0) return BD_ATTN_OK;  // packed layout with no tokens: nothing to read or write
   if (!dO || !Q || !K || !V || !O || !LSE || !dQ || !dK || !dV || (w.total > 0 && !ws))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(dO, 16) || !aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
@@ -323,10 +384,9 @@ int bwd_impl(const void* dO, const void* Q, const void* K, const void* V, const 
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (ws_bytes < w.total) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const size_t esz = dtype == BD_ATTN_FP32 ? 4 : 2;
-  const size_t N = 2 * (size_t)L;
-  const size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+  const size_t nq = q_rows(s) * s.D, nk = k_rows(s) * s.D;
   const Range in[] = {{dO, nq * esz}, {Q, nq * esz}, {K, nk * esz}, {V, nk * esz}, {O, nq * esz},
-                      {LSE, (size_t)B * Hq * N * 4}};
+                      {LSE, q_rows(s) * 4}};
   const Range out[] = {{dQ, nq * esz}, {dK, nk * esz}, {dV, nk * esz}, {ws, w.total}};
   for (const Range& o : out)
     for (const Range& i : in)

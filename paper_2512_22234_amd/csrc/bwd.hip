@@ -47,9 +47,11 @@ struct DkvParams {
   const float* rs;  // (lse2, delta) per query row
   bf16* dK;
   bf16* dV;
-  float* part;  // [2 (dK, dV)][B*Hkv][L][D]: unscaled sums of the half of a clean key tile's walk that finished first
+  float* part;  // [2 (dK, dV)][clean-half key rows][D]: unscaled sums of the half of a clean key tile's walk that finished first
   int* pair;    // per (clean key tile, key group): arrival count and ready flag, zeroed by the dq kernel
-  int L, S, Hq, Hkv, G, nKT, nkv;
+  SeqLayout seq;
+  size_t seq_clean_rows;           // rows of one plane of `part`: clean-half keys of every sequence and KV head
+  int L, S, Hq, Hkv, G, nKT, nkv;  // L: the (maximum) sequence length; nkv: sequences x KV heads
   float c;      // scale * log2(e)
   float scale;
 };
@@ -99,7 +101,6 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = w & 3;  // key group
   const int l32 = lane & 31, g2 = lane >> 5;
-  const int L = p.L, S = p.S, N = 2 * L;
 
   // Items: clean key tiles in ascending index (most work first), each as two
   // halves of its walk; then noisy key tiles, one item each.  Consecutive
@@ -112,12 +113,22 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int j = clean ? (rank >> 1) : rank - 2 * p.nKT;
   const int split = clean ? (rank & 1) : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
+  // sequence b: its length and where its rows lie
+  int L;
+  size_t qrow0, krow0, hrows;
+  p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
+  if (j * BN >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
+  // (a sequence shorter than S is one block: every formula below gives
+  // the S = L mask then)
+  const int S = p.S;
+  const int N = 2 * L;
   const int k0 = j * BN, k1 = imin(L, k0 + BN);
+  const size_t khead = krow0 + hk * hrows;  // row of this KV head's position 0 in K, V, dK, dV
 
   const int kk = k0 + kg * 32 + l32;  // this lane's key (local to its half)
   const bool kvalid = kk < k1;
   const int kblock0 = kvalid ? (kk / S) * S : 0;
-  const size_t krow = (size_t)grp * N + kh * L + kk;
+  const size_t krow = khead + kh * L + kk;
 
   const QueryWalk wk = query_walk(kh, j, split, L, S, BM, BN, p.G);
   const int T = wk.steps();
@@ -229,13 +240,13 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // row pairs each (the same data), so every wave issues NC instructions.
     // Addresses: the group's first query head is fixed, so a step adds one
     // row offset (head g, packed row row0) to three base pointers.
-    const size_t g0row = ((size_t)b * p.Hq + (size_t)hk * p.G) * N;  // first row of the group's first head
+    const size_t g0row = qrow0 + (size_t)hk * p.G * hrows;  // first row of the group's first head
     const bf16* const qg = p.Q + g0row * D;
     const bf16* const dog = p.dO + g0row * D;
     const float* const rsg = p.rs + 2 * g0row;
     auto issue = [&](WalkPos wp, char* dst) {
       const int row0 = wp.qh * L + wp.tile(wk) * BM;
-      const size_t r = (size_t)wp.g * N + row0;  // row within the group's heads
+      const size_t r = (size_t)wp.g * hrows + row0;  // row within the group's heads
       const int left = N - row0;                 // rows of this head from row0 on
       copy.issue_rows(qg + r * D, left, dst);
       copy.issue_rows(dog + r * D, left, dst + Smem::DO_OFF);
@@ -307,7 +318,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
 
     const float sc = isdk ? p.scale : 1.f;
     bf16* const outp = isdk ? p.dK : p.dV;
-    const size_t orow = (size_t)grp * N + kh * L;  // first row of this KV head's half
+    const size_t orow = khead + kh * L;  // first row of this KV head's half
     if (clean) {
       // The two halves of this key tile's walk meet here, per consumer wave:
       // the first to arrive stores its float32 sums and raises the ready
@@ -324,8 +335,9 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       // whole L2 under the workgroups still running.
       int* cnt = p.pair + 2 * ((j * p.nkv + grp) * 4 + c);
       int* ready = cnt + 1;
-      const size_t plane = (size_t)p.nkv * L * D;
-      const float* pbase = p.part + (isdk ? 0 : plane) + (size_t)grp * L * D;  // this KV head's rows
+      // one row per clean-half key: this head's clean keys start at row khead / 2
+      const size_t plane = (size_t)p.seq_clean_rows * D;
+      const float* pbase = p.part + (isdk ? 0 : plane) + (khead / 2) * D;
       const __amdgpu_buffer_rsrc_t pr = make_buffer(pbase, (uint32_t)(L * D * 4));
       constexpr int SC1 = 16;  // cache-policy bit: device scope
       int order = 0;
@@ -404,6 +416,7 @@ struct DqParams {
   int* pair;  // dK/dV pairing counters, cleared here
   int npair;
   bf16* dQ;
+  SeqLayout seq;
   int L, S, Hq, Hkv, G, nQT, nbh;
   float c;
   float scale;
@@ -427,22 +440,31 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
-  const int L = p.L, S = p.S, N = 2 * L;
 
   const int id = blockIdx.x;
+  for (int i = id * 256 + tid; i < p.npair; i += gridDim.x * 256) p.pair[i] = 0;
   const int rank = id / p.nbh;
   const int bh = xcd_head_remap(id - rank * p.nbh, p.nbh, p.G);
   const int qi = p.nQT - 1 - (rank >> 1);
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
+  // sequence b: its length and where its rows lie
+  int L;
+  size_t qrow0, krow0, hrows;
+  p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
+  if (qi * BM >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
+  // (a sequence shorter than S is one block: every formula below gives
+  // the S = L mask then)
+  const int S = p.S;
+  const int N = 2 * L;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
-  const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
+  const size_t kvbase = (krow0 + hk * hrows) * D;
 
   const int r = q0 + w * 32 + l32;
   const bool qvalid = r < q1;
   const int qblock0 = qvalid ? (r / S) * S : 0;
   const int prow = qh * L + r;
-  const size_t qrow = (size_t)bh * N + prow;
+  const size_t qrow = qrow0 + hq * hrows + prow;
 
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
   const int T = kl.count();
@@ -480,7 +502,6 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     const f32x2 v = {lse2, dlt};
     *reinterpret_cast<f32x2*>(p.rs + 2 * qrow) = v;
   }
-  for (int i = id * 256 + tid; i < p.npair; i += gridDim.x * 256) p.pair[i] = 0;
 
   const LdsOperands<D> ops(lane);
   f32x16 dqacc[DB];
@@ -493,10 +514,9 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   __syncthreads();
 
   // Per-step bookkeeping as in the forward kernel: a two-comparison FULL
-  // test and the visibility windows of both key halves computed once.
+  // test (the visibility window is only needed, and computed, on PARTIAL
+  // tiles: this kernel has no registers to spare for caching it).
   const FullRange fr = full_range_vs_query_tile(qh, q0, q1, L, S, BM);
-  const PosWindow win_n = keys_visible_from(qh, HALF_NOISY, qblock0, L, S, qvalid);
-  const PosWindow win_c = keys_visible_from(qh, HALF_CLEAN, qblock0, L, S, qvalid);
 
   // One key tile; restrict-qualified current and next buffers as in the
   // forward kernel, so the copy in flight does not make the compiler wait
@@ -541,7 +561,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       // the copy spread between the MFMAs
       pipeline_reads_and_copies<2 * DS * KB, 4, 1, DQ_COPIES>();
       // dS = P (dP - delta); FULL tiles without the per-element visibility test
-      const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
+      const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
       const unsigned span = (unsigned)(win.hi - win.lo);
       const int rel = k0 + 4 * g2 - win.lo;
       auto ds = [&](auto masked) __attribute__((always_inline)) {
@@ -604,6 +624,8 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.dV = static_cast<bf16*>(dV);
   p.part = part;
   p.pair = pair;
+  p.seq = s.seq;
+  p.seq_clean_rows = dkdv_clean_rows(s);
   p.L = s.L;
   p.S = s.S;
   p.Hq = s.Hq;
@@ -631,6 +653,7 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
   p.rs = rs;
   p.pair = pair;
   p.npair = (int)dkdv_pair_ints(s.B, s.Hkv, s.L);
+  p.seq = s.seq;
   p.dQ = static_cast<bf16*>(dQ);
   p.L = s.L;
   p.S = s.S;

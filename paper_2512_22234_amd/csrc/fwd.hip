@@ -29,7 +29,8 @@ struct FwdParams {
   const bf16* V;
   bf16* O;
   float* LSE;
-  int L, S, Hq, Hkv, G, nQT, nbh;
+  SeqLayout seq;
+  int L, S, Hq, Hkv, G, nQT, nbh;  // L: the (maximum) sequence length; nbh: sequences x query heads
   float c;  // scale * log2(e)
 };
 
@@ -57,7 +58,6 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, g2 = lane >> 5;
-  const int L = p.L, S = p.S, N = 2 * L;
 
   // Heaviest query tiles first (work grows with the tile index), noisy before
   // clean; heads remapped so a KV group stays on one XCD.
@@ -67,9 +67,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int qi = p.nQT - 1 - (rank >> 1);
   const int qh = rank & 1;
   const int b = bh / p.Hq, hq = bh - b * p.Hq, hk = hq / p.G;
+  // sequence b: its length and where its rows lie
+  int L;
+  size_t qrow0, krow0, hrows;
+  p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
+  if (qi * BM >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
+  // (a sequence shorter than S is one block: every formula below gives
+  // the S = L mask then)
+  const int S = p.S;
+  const int N = 2 * L;
   const int q0 = qi * BM, q1 = imin(L, q0 + BM);
 
-  const size_t kvbase = (size_t)(b * p.Hkv + hk) * N * D;
+  const size_t kvbase = (krow0 + hk * hrows) * D;
+  const size_t qbase = qrow0 + hq * hrows;  // row of this head's position 0 in Q, O and LSE
 
   const int r = q0 + w * 32 + l32;  // this lane's query row (local to its half)
   const bool qvalid = r < q1;
@@ -100,7 +110,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 
   bf16x8 qreg[DS];
   {
-    const bf16* qp = p.Q + ((size_t)bh * N + prow) * D + 8 * g2;
+    const bf16* qp = p.Q + (qbase + prow) * D + 8 * g2;
 #pragma unroll
     for (int s = 0; s < DS; ++s)
       qreg[s] = qvalid ? *reinterpret_cast<const bf16x8*>(qp + 16 * s) : zero_bf16x8();
@@ -228,14 +238,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const float lt = halves_sum(lsum);
   if (qvalid) {
     const float inv = 1.f / lt;
-    bf16* op = p.O + ((size_t)bh * N + prow) * D + 4 * g2;
+    bf16* op = p.O + (qbase + prow) * D + 4 * g2;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         st_bf16x4(op + db * 32 + 8 * i, oacc[db][4 * i] * inv, oacc[db][4 * i + 1] * inv,
                   oacc[db][4 * i + 2] * inv, oacc[db][4 * i + 3] * inv);
-    if (g2 == 0) p.LSE[(size_t)bh * N + prow] = (m + log2f(lt)) * LN2;
+    if (g2 == 0) p.LSE[qbase + prow] = (m + log2f(lt)) * LN2;
   }
 }
 
@@ -248,6 +258,7 @@ hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void
   p.V = static_cast<const bf16*>(V);
   p.O = static_cast<bf16*>(O);
   p.LSE = LSE;
+  p.seq = s.seq;
   p.L = s.L;
   p.S = s.S;
   p.Hq = s.Hq;

@@ -7,10 +7,40 @@
 
 namespace bd {
 
+// Where the sequences lie in the Q-like ([.., Hq, .., D]) and K-like
+// ([.., Hkv, .., D]) arrays.
+//   Fixed length (cu == nullptr): B sequences of length L; arrays
+//     [B][H][2L][D], sequence s's head h at rows (s*H + h)*2L.
+//   Packed (cu != nullptr): B sequences with cumulative lengths cu[0..B]
+//     (device int32, cu[0] = 0, total T = cu[B]); arrays [H][2T][D],
+//     sequence s occupying rows [2 cu[s], 2 cu[s+1]) of every head.  L is
+//     then an upper bound on every length (it sizes the grids).
+struct SeqLayout {
+  const int* cu;
+  int T;
+  // Length of sequence s, and the first row of its head 0 in the Q-like and
+  // the K-like arrays; heads are `hrows` rows apart.
+  __device__ void get(int s, int L, int Hq, int Hkv, int& Ls, size_t& qrow, size_t& krow, size_t& hrows) const {
+    if (cu == nullptr) {
+      Ls = L;
+      hrows = 2 * (size_t)L;
+      qrow = (size_t)s * Hq * hrows;
+      krow = (size_t)s * Hkv * hrows;
+    } else {
+      // the same for every lane: keep it (and all addresses derived from it) scalar
+      const int c0 = __builtin_amdgcn_readfirstlane(cu[s]);
+      Ls = __builtin_amdgcn_readfirstlane(cu[s + 1]) - c0;
+      hrows = 2 * (size_t)T;
+      qrow = krow = 2 * (size_t)c0;
+    }
+  }
+};
+
 struct Shape {
-  int B, L, S, Hq, Hkv, D;
-  int G;        // Hq / Hkv
-  float scale;  // softmax scale (already resolved)
+  int B, L, S, Hq, Hkv, D;  // B sequences of length L (packed: B sequences, L bounds their lengths)
+  int G;                    // Hq / Hkv
+  float scale;              // softmax scale (already resolved)
+  SeqLayout seq;
 };
 
 // Forward tiles: BM queries per workgroup (4 waves x 32), BN keys per step.
@@ -39,10 +69,15 @@ hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const v
                            const void* dO, const float* rs, void* dK, void* dV, float* part, int* pair,
                            hipStream_t st);
 
-// float32 sums of one half of the clean key tiles' walks: dK and dV.
-inline size_t dkdv_partial_floats(int B, int Hkv, int L, int D) {
-  return (size_t)2 * B * Hkv * L * D;
+// Clean-half key rows of every sequence and KV head: B*Hkv*L for fixed
+// length, Hkv*T packed.  Row khead / 2 + k is key k of the clean half of the
+// KV head whose position 0 is at K row khead.
+inline size_t dkdv_clean_rows(const Shape& s) {
+  return s.seq.cu ? (size_t)s.Hkv * s.seq.T : (size_t)s.B * s.Hkv * s.L;
 }
+// float32 sums of one half of the clean key tiles' walks: dK and dV, one row
+// per clean-half key.
+inline size_t dkdv_partial_floats(const Shape& s) { return 2 * dkdv_clean_rows(s) * s.D; }
 // Pairing counters: per (clean key tile, batch x KV head, key group of 32) an
 // arrival count and a ready flag.
 inline size_t dkdv_pair_ints(int B, int Hkv, int L) {

@@ -94,3 +94,48 @@ def make_random_case(B, Hq, Hkv, D, L, S, seed, dtype="bf16", amp=0.5):
     """Inputs for an arbitrary shape (parity sweeps and edge cases)."""
     w = Workload("case", B, Hq, Hkv, D, L, S, seed=seed, dtype=dtype, amp=amp)
     return make_inputs(w)
+
+
+# ---------------------------------------------------------------------------
+# Packed sequences (several [x_t | x_0] pairs of different lengths in one
+# buffer, the dynamic packing of Section 5.2).
+
+def varlen_lengths(total: int, seed: int, lo: int = 64, hi: int = 2048) -> list:
+    """Sequence lengths (tokens per copy) summing to `total`: log-uniform draws
+    in [lo, hi] from a seeded generator, the last one cut to fit.  RL rollouts
+    of different lengths packed into one training buffer look like this."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    out, left = [], total
+    while left > 0:
+        u = float(torch.rand((), generator=g))
+        n = int(round(lo * (hi / lo) ** u))
+        n = max(1, min(n, left))
+        out.append(n)
+        left -= n
+    return out
+
+
+def make_varlen_inputs(lengths, Hq: int, Hkv: int, D: int, seed: int, dtype: str = "bf16", amp: float = 0.5):
+    """CPU tensors q [Hq, 2T, D], k, v [Hkv, 2T, D], do [Hq, 2T, D] and
+    cu_seqlens (int32, len(lengths) + 1): N(0,1)*amp inputs and N(0,1) dO
+    drawn in the order q, k, v, dO from a seeded generator, then rounded."""
+    T = int(sum(lengths))
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    q = torch.randn((Hq, 2 * T, D), generator=g) * amp
+    k = torch.randn((Hkv, 2 * T, D), generator=g) * amp
+    v = torch.randn((Hkv, 2 * T, D), generator=g) * amp
+    do = torch.randn((Hq, 2 * T, D), generator=g)
+    cu = torch.zeros(len(lengths) + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(torch.tensor(lengths, dtype=torch.int64), 0).to(torch.int32)
+    dt = torch_dtype(dtype)
+    return q.to(dt), k.to(dt), v.to(dt), do.to(dt), cu
+
+
+# The packed workload measured beside the 8B batch: the same heads, head size
+# and block size, 4096 tokens per copy in all (as many as the 8B batch of two
+# 2048-token sequences) split into sequences of 64..2048 tokens.
+VARLEN_WORKLOADS = {
+    "8b_packed": dict(total=4096, Hq=32, Hkv=8, D=128, S=4, seed=8, lo=64, hi=2048),
+}
