@@ -4,10 +4,11 @@
 One step = bd_attn_fwd + bd_attn_bwd over one batch of the 8B-shaped training
 workload (B=2, Hq=32, Hkv=8, D=128, L=2048 so 4096 packed tokens, S=4, bf16
 N(0,1)*0.5 inputs, dO ~ N(0,1)), inputs resident in HBM (warm caches: the
-working set fits the 256 MB Infinity Cache).  W untimed warm-up steps (10),
-then K timed steps (50) bracketed by device synchronisation and HIP events on
-the stream the library runs on; the per-step median is reported beside the
-mean.
+working set fits the 256 MB Infinity Cache).  W untimed warm-up steps (100,
+about 75 ms: the GPU's clocks settle only after tens of milliseconds under
+load), then K timed steps (50) bracketed by device synchronisation and HIP
+events on the stream the library runs on; the per-step median is reported
+beside the mean.
 
 value  = effective TFLOP/s counting only visible (query, key) pairs:
          (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
@@ -17,6 +18,9 @@ roofline: the dominant kernel's algorithmic FLOPs per launch over its average
          steps, against the bf16 dense MFMA peak.
 cpu_baseline: the fp64 oracle (test infrastructure) timed on the host cores on
          a bounded sample of the same workload (whole GQA groups).
+packed:  the same step over packed sequences of mixed lengths (the same heads,
+         4096 tokens per copy in all) through the varlen calls, reported
+         beside the headline (not part of `value`).
 
 Prints exactly one JSON line on stdout; details go to stderr.
 """
@@ -134,13 +138,54 @@ def cpu_baseline(w, budget_s: float, max_groups: int):
                       f"fwd+bwd in fp64 numpy ({blas} BLAS), {t_total:.1f} s; same visible-pair FLOP count"}
 
 
+def packed_step(steps: int, warmup: int, name: str = "8b_packed"):
+    """fwd+bwd over packed sequences (varlen calls): effective TFLOP/s with the
+    same visible-pair FLOP count as the headline, summed over the sequences."""
+    import torch
+    import paper_2512_22234_amd as bd
+    from paper_2512_22234_amd.workloads import VARLEN_WORKLOADS, make_varlen_inputs, varlen_lengths
+    c = VARLEN_WORKLOADS[name]
+    lengths = varlen_lengths(c["total"], c["seed"], c["lo"], c["hi"])
+    dev = torch.device("cuda:0")
+    q, k, v, do, cu = (t.to(dev) for t in make_varlen_inputs(lengths, c["Hq"], c["Hkv"], c["D"], c["seed"]))
+    max_L, S, T = max(lengths), c["S"], sum(lengths)
+    code = bd.BD_ATTN_BF16
+    o, lse = torch.empty_like(q), torch.empty((c["Hq"], 2 * T), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    wsb = torch.empty(bd.bd_attn_varlen_workspace_bytes(len(lengths), T, max_L, S, c["Hq"], c["Hkv"], c["D"],
+                                                        code, 1), dtype=torch.uint8, device=dev)
+
+    def step():
+        bd.bd_attn_varlen_fwd(q, k, v, cu, max_L, S, out=o, lse=lse)
+        bd.bd_attn_varlen_bwd(do, q, k, v, o, lse, cu, max_L, S, dq=dq, dk=dk, dv=dv, workspace=wsb)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    npairs = sum(visible_pairs(Li, S) for Li in lengths) * c["Hq"]
+    tflops = 14 * c["D"] * npairs / (ms * 1e-3) / 1e12
+    log(f"[bench] packed {name}: {len(lengths)} sequences {lengths}, {ms:.4f} ms/step, {tflops:.1f} TFLOP/s eff")
+    return {"workload": f"{name}: {len(lengths)} packed sequences of {lengths} tokens per copy "
+                        f"(T={T}), Hq={c['Hq']} Hkv={c['Hkv']} D={c['D']} S={S}, bf16, fwd+bwd",
+            "ms_per_step": round(ms, 5), "tflops_eff": round(tflops, 2),
+            "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-packed", action="store_true", help="skip the packed-sequence measurement")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
     ap.add_argument("--cpu-max-groups", type=int, default=4)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -238,6 +283,8 @@ def main():
     log(f"[bench] fwd {t_fwd:.4f} ms ({f_fwd / t_fwd / 1e9:.1f} TFLOP/s eff), bwd {t_bwd:.4f} ms "
         f"({f_bwd / t_bwd / 1e9:.1f} TFLOP/s eff at 10D, {f_bwd8 / t_bwd / 1e9:.1f} at 8D)")
 
+    packed = None if args.no_packed else packed_step(args.steps, args.warmup)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_budget, args.cpu_max_groups)
@@ -268,6 +315,7 @@ def main():
                      "traffic": measured_traffic(dom, w.name), "traffic_unit": "HBM bytes per launch",
                      "algorithmic_flops_per_launch": alg[dom]},
         "kernels": kernels,
+        "packed": packed,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
