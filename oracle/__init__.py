@@ -15,4 +15,5 @@ from .bd_attn_oracle import (  # noqa: F401
     varlen_visibility_mask,
     varlen_forward,
     varlen_backward,
+    decode_forward,
 )

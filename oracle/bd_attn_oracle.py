@@ -314,3 +314,38 @@ def varlen_backward(dO, Q, K, V, lengths, S: int, scale: float | None = None):
         dK[g] += scale * (dS.T @ Q[h])
         dV[g] += P.T @ dO[h]
     return dQ, dK, dV
+
+
+# ---------------------------------------------------------------------------
+# Decoding (rollouts): the KV-cache reading of Section 2.1.  While block k is
+# denoised, its S noisy tokens attend to the clean tokens of the blocks
+# before it, held in a KV cache, and to each other in both directions (Eq. 2);
+# nothing else exists yet.  So the noisy rows of block k see every cached key
+# and every key of their own block, with no further mask.
+
+def decode_forward(Q, Kc, Vc, Kn, Vn, cache_lens, scale: float | None = None):
+    """O [B,Hq,S,D] and LSE [B,Hq,S] of one block's noisy queries Q [B,Hq,S,D]
+    over the clean cache Kc/Vc [B,Hkv,C,D] (the first cache_lens[b] rows of
+    sequence b are valid) and the block's own noisy keys Kn/Vn [B,Hkv,S,D]:
+    dense softmax attention over the concatenation [cache ; block]."""
+    Q, Kc, Vc, Kn, Vn = _as64(Q), _as64(Kc), _as64(Vc), _as64(Kn), _as64(Vn)
+    B, Hq, S, D = Q.shape
+    Hkv = Kc.shape[1]
+    if Hq % Hkv or Kn.shape != (B, Hkv, S, D) or Vn.shape != Kn.shape or Vc.shape != Kc.shape:
+        raise ValueError("inconsistent shapes")
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(D) if scale is None or scale <= 0 else float(scale)
+    O = np.zeros(Q.shape)
+    LSE = np.zeros(Q.shape[:3])
+    for b in range(B):
+        n = int(cache_lens[b])
+        if not 0 <= n <= Kc.shape[2]:
+            raise ValueError("cache length out of range")
+        for h in range(Hq):
+            g = h // G
+            Kall = np.concatenate([Kc[b, g, :n], Kn[b, g]], axis=0)
+            Vall = np.concatenate([Vc[b, g, :n], Vn[b, g]], axis=0)
+            P, m, l = _softmax_rows(scale * (Q[b, h] @ Kall.T), np.ones((S, n + S), dtype=bool))
+            O[b, h] = P @ Vall
+            LSE[b, h] = (m + np.log(l))[:, 0]
+    return O, LSE

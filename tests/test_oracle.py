@@ -14,7 +14,10 @@
 * packed sequences (varlen): the packed mask against plain pair-by-pair loops,
   one sequence against the single-sequence mask, equal lengths against the
   batched oracle, each sequence against its own batched call, independence of
-  the sequences, and finite differences.
+  the sequences, and finite differences;
+* decoding: the noisy rows of block k of the training forward pass (the
+  KV-cache view of Section 2.1), torch SDPA over the concatenated keys, and
+  cache rows past the length having no effect.
 """
 import math
 import os
@@ -447,3 +450,49 @@ def test_varlen_backward_finite_differences():
             args_m = [Xm if Y is X else Y for Y in (Q, K, V)]
             fd = (f(*args_p) - f(*args_m)) / (2 * h)
             assert abs(fd - G[idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, G[idx])
+
+
+# ------------------------------------------------------------- decoding
+
+def test_decode_equals_noisy_rows_of_the_training_mask():
+    """The KV-cache view of Section 2.1: with the cache holding the clean K/V
+    of blocks 0..k-1, decoding block k gives exactly the noisy rows of block k
+    of the training forward pass (whose mask sees the same keys)."""
+    S, D, Hq, Hkv = 4, 8, 4, 2
+    for L, k in ((16, 0), (16, 2), (16, 3), (14, 3)):   # L=14: a shorter last block
+        Q, K, V = _rand((1, Hq, 2 * L, D), 50 + k), _rand((1, Hkv, 2 * L, D), 60 + k), _rand((1, Hkv, 2 * L, D), 70 + k)
+        O, LSE = oracle.forward(Q, K, V, L, S)
+        a, e = k * S, min(L, (k + 1) * S)
+        C = L
+        Kc = np.zeros((1, Hkv, C, D)); Vc = np.zeros((1, Hkv, C, D))
+        Kc[:, :, :a] = K[:, :, L:L + a]
+        Vc[:, :, :a] = V[:, :, L:L + a]
+        Od, LSEd = oracle.decode_forward(Q[:, :, a:e], Kc, Vc, K[:, :, a:e], V[:, :, a:e], [a])
+        np.testing.assert_allclose(Od, O[:, :, a:e], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(LSEd, LSE[:, :, a:e], rtol=1e-12, atol=1e-12)
+
+
+def test_decode_matches_torch_sdpa_over_the_concatenation():
+    B, Hq, Hkv, S, D, C = 3, 4, 1, 5, 16, 12
+    Q, Kc, Vc = _rand((B, Hq, S, D), 80), _rand((B, Hkv, C, D), 81), _rand((B, Hkv, C, D), 82)
+    Kn, Vn = _rand((B, Hkv, S, D), 83), _rand((B, Hkv, S, D), 84)
+    lens = [0, 7, 12]
+    O, LSE = oracle.decode_forward(Q, Kc, Vc, Kn, Vn, lens)
+    for b, n in enumerate(lens):
+        kk = torch.from_numpy(np.concatenate([Kc[b, :, :n], Kn[b]], axis=1)).repeat_interleave(Hq // Hkv, 0)
+        vv = torch.from_numpy(np.concatenate([Vc[b, :, :n], Vn[b]], axis=1)).repeat_interleave(Hq // Hkv, 0)
+        ref = F.scaled_dot_product_attention(torch.from_numpy(Q[b])[None], kk[None], vv[None])[0].numpy()
+        np.testing.assert_allclose(O[b], ref, rtol=1e-10, atol=1e-12)
+        z = (Q[b] @ np.swapaxes(np.concatenate([Kc[b, :, :n], Kn[b]], axis=1), 1, 2).repeat(Hq // Hkv, 0)) / math.sqrt(D)
+        np.testing.assert_allclose(LSE[b], np.log(np.exp(z).sum(-1)), rtol=1e-12, atol=1e-12)
+
+
+def test_decode_ignores_cache_rows_past_the_length():
+    B, Hq, Hkv, S, D, C = 1, 2, 1, 3, 8, 10
+    Q, Kc, Vc = _rand((B, Hq, S, D), 90), _rand((B, Hkv, C, D), 91), _rand((B, Hkv, C, D), 92)
+    Kn, Vn = _rand((B, Hkv, S, D), 93), _rand((B, Hkv, S, D), 94)
+    O1, _ = oracle.decode_forward(Q, Kc, Vc, Kn, Vn, [6])
+    Kc[:, :, 6:] = 1e3
+    Vc[:, :, 6:] = -1e3
+    O2, _ = oracle.decode_forward(Q, Kc, Vc, Kn, Vn, [6])
+    np.testing.assert_array_equal(O1, O2)
