@@ -21,6 +21,11 @@ cpu_baseline: the fp64 oracle (test infrastructure) timed on the host cores on
 packed:  the same step over packed sequences of mixed lengths (the same heads,
          4096 tokens per copy in all) through the varlen calls, reported
          beside the headline (not part of `value`).
+decode:  one block-decoding call over a KV cache (64 rollouts of the 8B
+         shape, caches of 512..8192 tokens, blocks of 4): HBM bytes the call
+         must move (cached K/V rows up to each length, the block's K/V, Q, O,
+         LSE) over its duration, against the 8 TB/s HBM peak (not part of
+         `value`).
 
 Prints exactly one JSON line on stdout; details go to stderr.
 """
@@ -178,6 +183,49 @@ def packed_step(steps: int, warmup: int, name: str = "8b_packed"):
             "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 3)}
 
 
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+
+
+def decode_step(steps: int, warmup: int, name: str = "8b_decode"):
+    """bd_attn_decode_fwd over a rollout batch: algorithmic HBM GB/s."""
+    import torch
+    import paper_2512_22234_amd as bd
+    from paper_2512_22234_amd.workloads import DECODE_WORKLOADS, decode_cache_lens, make_decode_inputs
+    c = DECODE_WORKLOADS[name]
+    lens = decode_cache_lens(c["B"], c["seed"], c["lo"], c["hi"])
+    B, Hq, Hkv, D, S, C = c["B"], c["Hq"], c["Hkv"], c["D"], c["S"], c["capacity"]
+    q, kc, vc, kn, vn, cl = make_decode_inputs(B, Hq, Hkv, D, S, C, lens, seed=c["seed"], device="cuda")
+    max_len = max(lens)
+    o, lse = torch.empty_like(q), torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
+    ws = torch.empty(max(bd.bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, C, max_len), 16), dtype=torch.uint8,
+                     device=q.device)
+
+    def call():
+        bd.bd_attn_decode_fwd(q, kc, vc, kn, vn, cl, max_len=max_len, out=o, lse=lse, workspace=ws)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = (sum(lens) * Hkv * D * 2 * 2          # cached K and V rows, bf16
+              + B * Hkv * S * D * 2 * 2            # the block's K and V
+              + 2 * B * Hq * S * D * 2             # Q in, O out
+              + B * Hq * S * 4)                    # LSE out
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    log(f"[bench] decode {name}: cache lengths {min(lens)}..{max(lens)} (mean {sum(lens) / B:.0f}), "
+        f"{ms * 1e3:.1f} us/call, {nbytes / 1e6:.1f} MB, {gbs:.0f} GB/s")
+    return {"workload": f"{name}: B={B} Hq={Hq} Hkv={Hkv} D={D} S={S}, capacity {C}, cache lengths "
+                        f"log-uniform {c['lo']}..{c['hi']} (sum {sum(lens)}), bf16",
+            "us_per_call": round(ms * 1e3, 2), "algorithmic_bytes": nbytes, "gbs": round(gbs, 1),
+            "peak_gbs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -186,6 +234,7 @@ def main():
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-packed", action="store_true", help="skip the packed-sequence measurement")
+    ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
     ap.add_argument("--cpu-max-groups", type=int, default=4)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -284,6 +333,7 @@ def main():
         f"({f_bwd / t_bwd / 1e9:.1f} TFLOP/s eff at 10D, {f_bwd8 / t_bwd / 1e9:.1f} at 8D)")
 
     packed = None if args.no_packed else packed_step(args.steps, args.warmup)
+    decode = None if args.no_decode else decode_step(args.steps, args.warmup)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -316,6 +366,7 @@ def main():
                      "algorithmic_flops_per_launch": alg[dom]},
         "kernels": kernels,
         "packed": packed,
+        "decode": decode,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -182,6 +182,46 @@ int bd_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void*
 size_t bd_attn_varlen_workspace_bytes(int n_seqs, int total_L, int max_L, int S, int Hq, int Hkv, int D,
                                       int dtype, int for_bwd);
 
+/*
+ * Block decoding over a KV cache (Section 2.1: blockwise models keep the
+ * K/V of finished blocks in a cache; the block being denoised attends to
+ * that cache and, in both directions, to itself, Eq. 2).  For each sequence
+ * b and query head h, the S noisy queries of the current block attend to the
+ * first cache_lens[b] rows of the KV head's cache followed by the block's
+ * own S keys, with no further mask: the noisy rows of the training mask of
+ * Section 4.1 for a block whose earlier blocks are all cached.
+ *
+ * Layouts (contiguous, innermost last, bfloat16, 16-byte aligned):
+ *   Q, O             : [B, Hq, S, D]
+ *   K_cache, V_cache : [B, Hkv, capacity, D]   (rows past cache_lens[b] are not read)
+ *   K_new, V_new     : [B, Hkv, S, D]          (the block's own keys and values)
+ *   LSE              : [B, Hq, S] float32, natural-log log-sum-exp of the
+ *                      scaled scores of each row.
+ * cache_lens: DEVICE array of B int32 values (4-byte aligned), read by the
+ *   kernels only.  Each must lie in [0, max_len]; values outside are clamped
+ *   to that range.  max_len <= capacity <= 2^22 is a host-side bound that
+ *   sizes the launch (max_len = capacity is always correct; a tighter bound
+ *   launches fewer idle workgroups).  capacity = 0 allows NULL caches.
+ * dtype: BD_ATTN_BF16 only (anything else is BD_ATTN_ERR_UNSUPPORTED).
+ * keys_per_split: 0 lets the library choose how many keys one workgroup
+ *   streams; otherwise a positive multiple of 32.  Longer caches are split
+ *   into that many keys per workgroup, and a second kernel merges the splits'
+ *   softmax states (the result depends on the split only through float32
+ *   rounding).
+ * ws/ws_bytes: device workspace of at least bd_attn_decode_workspace_bytes
+ *   bytes for the same arguments (0 when no sequence needs more than one
+ *   split; ws may then be NULL).
+ * Ownership, stream order and errors are as for bd_attn_fwd.
+ */
+int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, const void* K_new,
+                       const void* V_new, const int32_t* cache_lens, int B, int S, int Hq, int Hkv, int D,
+                       int capacity, int max_len, float scale, int dtype, int keys_per_split,
+                       void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Workspace bytes for bd_attn_decode_fwd; 0 for arguments it would reject
+ * and when it needs none. */
+size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int max_len,
+                                      int dtype, int keys_per_split);
+
 /* Comma-separated names of the kernels bd_attn_fwd (for_bwd = 0) or
  * bd_attn_bwd (for_bwd = 1) launch for `dtype`, in launch order (static). */
 const char* bd_attn_stage_names(int for_bwd, int dtype);

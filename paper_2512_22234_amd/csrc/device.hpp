@@ -269,8 +269,9 @@ __device__ inline void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70);
 // (loads complete in issue order for this counter).
 template <int N>
 __device__ inline void wait_global_loads_but() {
-  static_assert(N >= 0 && N < 16, "vmcnt immediate");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
+  // vmcnt is split over bits 3:0 and 15:14 of the immediate
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 // Workgroup barrier that drains this wave's LDS operations (lgkmcnt(0)) but

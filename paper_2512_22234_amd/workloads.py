@@ -139,3 +139,46 @@ def make_varlen_inputs(lengths, Hq: int, Hkv: int, D: int, seed: int, dtype: str
 VARLEN_WORKLOADS = {
     "8b_packed": dict(total=4096, Hq=32, Hkv=8, D=128, S=4, seed=8, lo=64, hi=2048),
 }
+
+
+# ---------------------------------------------------------------------------
+# Block decoding over a KV cache (rollouts, Section 2.1): a batch of sequences
+# at different points of their generation, each denoising one block of S
+# tokens against the cached K/V of everything before it.
+
+def decode_cache_lens(B: int, seed: int, lo: int, hi: int) -> list:
+    """B cache lengths, log-uniform in [lo, hi] from a seeded generator: a
+    rollout batch whose prompts and generated prefixes differ in length."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    u = torch.rand((B,), generator=g, dtype=torch.float64)
+    return [int(round(lo * (hi / lo) ** float(x))) for x in u]
+
+
+def make_decode_inputs(B: int, Hq: int, Hkv: int, D: int, S: int, capacity: int, cache_lens, seed: int,
+                       amp: float = 0.5, device: str = "cpu"):
+    """bf16 tensors q [B,Hq,S,D], k_cache, v_cache [B,Hkv,capacity,D], k_new,
+    v_new [B,Hkv,S,D] (N(0,1)*amp, drawn in that order from a generator seeded
+    with `seed` on `device`) and cache_lens (int32 [B], on `device`).  Cache
+    rows past a sequence's length hold draws too: nothing may read them."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+
+    def draw(*shape):
+        return (torch.randn(shape, generator=g, device=device) * amp).to(torch.bfloat16)
+
+    q = draw(B, Hq, S, D)
+    kc = draw(B, Hkv, capacity, D)
+    vc = draw(B, Hkv, capacity, D)
+    kn = draw(B, Hkv, S, D)
+    vn = draw(B, Hkv, S, D)
+    lens = torch.tensor([int(x) for x in cache_lens], dtype=torch.int32, device=device)
+    return q, kc, vc, kn, vn, lens
+
+
+# The decode workload measured beside the training step: 64 rollouts of the
+# 8B shape (32 query heads, 8 KV heads, D = 128, blocks of 4 tokens) with
+# caches of 512..8192 tokens (log-uniform), cache capacity 8192.
+DECODE_WORKLOADS = {
+    "8b_decode": dict(B=64, Hq=32, Hkv=8, D=128, S=4, capacity=8192, lo=512, hi=8192, seed=9),
+}
