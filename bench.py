@@ -195,13 +195,11 @@ def decode_step(steps: int, warmup: int, name: str = "8b_decode"):
     lens = decode_cache_lens(c["B"], c["seed"], c["lo"], c["hi"])
     B, Hq, Hkv, D, S, C = c["B"], c["Hq"], c["Hkv"], c["D"], c["S"], c["capacity"]
     q, kc, vc, kn, vn, cl = make_decode_inputs(B, Hq, Hkv, D, S, C, lens, seed=c["seed"], device="cuda")
-    max_len = max(lens)
     o, lse = torch.empty_like(q), torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
-    ws = torch.empty(max(bd.bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, C, max_len), 16), dtype=torch.uint8,
-                     device=q.device)
+    ws = torch.empty(bd.bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, C), dtype=torch.uint8, device=q.device)
 
     def call():
-        bd.bd_attn_decode_fwd(q, kc, vc, kn, vn, cl, max_len=max_len, out=o, lse=lse, workspace=ws)
+        bd.bd_attn_decode_fwd(q, kc, vc, kn, vn, cl, out=o, lse=lse, workspace=ws)
 
     for _ in range(warmup):
         call()

@@ -198,29 +198,23 @@ size_t bd_attn_varlen_workspace_bytes(int n_seqs, int total_L, int max_L, int S,
  *   LSE              : [B, Hq, S] float32, natural-log log-sum-exp of the
  *                      scaled scores of each row.
  * cache_lens: DEVICE array of B int32 values (4-byte aligned), read by the
- *   kernels only.  Each must lie in [0, max_len]; values outside are clamped
- *   to that range.  max_len <= capacity <= 2^22 is a host-side bound that
- *   sizes the launch (max_len = capacity is always correct; a tighter bound
- *   launches fewer idle workgroups).  capacity = 0 allows NULL caches.
+ *   kernels only (the host never waits for it).  Values are clamped to
+ *   [0, capacity].  capacity <= 2^22; capacity = 0 allows NULL caches.
  * dtype: BD_ATTN_BF16 only (anything else is BD_ATTN_ERR_UNSUPPORTED).
- * keys_per_split: 0 lets the library choose how many keys one workgroup
- *   streams; otherwise a positive multiple of 32.  Longer caches are split
- *   into that many keys per workgroup, and a second kernel merges the splits'
- *   softmax states (the result depends on the split only through float32
- *   rounding).
+ * The key tiles of all sequences and heads are shared out evenly over a
+ * fixed set of waves, whatever the lengths; a KV head's keys split over
+ * several waves are merged by a second kernel (the result depends on the
+ * lengths of the other sequences only through float32 rounding).
  * ws/ws_bytes: device workspace of at least bd_attn_decode_workspace_bytes
- *   bytes for the same arguments (0 when no sequence needs more than one
- *   split; ws may then be NULL).
+ *   bytes (16-byte aligned; it need not be initialised).
  * Ownership, stream order and errors are as for bd_attn_fwd.
  */
 int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, const void* K_new,
                        const void* V_new, const int32_t* cache_lens, int B, int S, int Hq, int Hkv, int D,
-                       int capacity, int max_len, float scale, int dtype, int keys_per_split,
-                       void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream);
-/* Workspace bytes for bd_attn_decode_fwd; 0 for arguments it would reject
- * and when it needs none. */
-size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int max_len,
-                                      int dtype, int keys_per_split);
+                       int capacity, float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes,
+                       hipStream_t stream);
+/* Workspace bytes for bd_attn_decode_fwd; 0 for arguments it would reject. */
+size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int dtype);
 
 /* Comma-separated names of the kernels bd_attn_fwd (for_bwd = 0) or
  * bd_attn_bwd (for_bwd = 1) launch for `dtype`, in launch order (static). */

@@ -316,19 +316,16 @@ def bd_attn_varlen(q, k, v, cu_seqlens, max_L: int, S: int, scale=None):
     return BdAttnVarlenFunction.apply(q, k, v, cu_seqlens, max_L, S, scale)
 
 
-def bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, capacity, max_len, dtype=BD_ATTN_BF16,
-                                   keys_per_split=0) -> int:
-    return int(lib().bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, capacity, max_len, int(dtype),
-                                                      int(keys_per_split)))
+def bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, capacity, dtype=BD_ATTN_BF16) -> int:
+    return int(lib().bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, capacity, int(dtype)))
 
 
-def bd_attn_decode_fwd(q, k_cache, v_cache, k_new, v_new, cache_lens, max_len=None, scale=None,
-                       keys_per_split: int = 0, out=None, lse=None, workspace=None, stream=None):
+def bd_attn_decode_fwd(q, k_cache, v_cache, k_new, v_new, cache_lens, scale=None, out=None, lse=None,
+                       workspace=None, stream=None):
     """One block's decoding step over a KV cache; returns (O [B,Hq,S,D], LSE [B,Hq,S] float32).
 
     q [B,Hq,S,D]; k_cache/v_cache [B,Hkv,C,D]; k_new/v_new [B,Hkv,S,D], all
-    bfloat16; cache_lens: int32 [B] on the device.  max_len bounds every cache
-    length (default C)."""
+    bfloat16; cache_lens: int32 [B] on the device (clamped to [0, C])."""
     if q.dim() != 4 or k_cache.dim() != 4:
         raise ValueError("q [B,Hq,S,D] and k_cache/v_cache [B,Hkv,C,D] expected")
     B, Hq, S, D = q.shape
@@ -340,17 +337,16 @@ def bd_attn_decode_fwd(q, k_cache, v_cache, k_new, v_new, cache_lens, max_len=No
                          ("k_new", k_new, (B, Hkv, S, D)), ("v_new", v_new, (B, Hkv, S, D))):
         _check(name, t, shp, torch.bfloat16, dev)
     _check("cache_lens", cache_lens, (B,), torch.int32, dev)
-    max_len = C if max_len is None else int(max_len)
     o = torch.empty_like(q) if out is None else out
     l_ = torch.empty((B, Hq, S), dtype=torch.float32, device=dev) if lse is None else lse
     _check("out", o, q.shape, torch.bfloat16, dev)
     _check("lse", l_, (B, Hq, S), torch.float32, dev)
-    nbytes = bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, C, max_len, BD_ATTN_BF16, keys_per_split)
+    nbytes = bd_attn_decode_workspace_bytes(B, S, Hq, Hkv, D, C, BD_ATTN_BF16)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
     s, sh = _stream(dev, stream)
     st = lib().bd_attn_decode_fwd(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_new), _ptr(v_new),
-                                  _ptr(cache_lens), B, S, Hq, Hkv, D, C, max_len, _scale_arg(scale),
-                                  BD_ATTN_BF16, int(keys_per_split), _ptr(o), _ptr(l_), _ptr(ws), ws.numel(), sh)
+                                  _ptr(cache_lens), B, S, Hq, Hkv, D, C, _scale_arg(scale), BD_ATTN_BF16,
+                                  _ptr(o), _ptr(l_), _ptr(ws), ws.numel(), sh)
     if st:
         raise BdAttnError(st, "bd_attn_decode_fwd")
     if stream is not None and workspace is None:

@@ -48,10 +48,9 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_varlen_workspace_bytes.restype = sz
     L.bd_attn_varlen_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ci]
     L.bd_attn_decode_fwd.restype = ci
-    L.bd_attn_decode_fwd.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, ci, ci,
-                                     vp, vp, vp, sz, vp]
+    L.bd_attn_decode_fwd.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci, vp, vp, vp, sz, vp]
     L.bd_attn_decode_workspace_bytes.restype = sz
-    L.bd_attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ci]
+    L.bd_attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci]
     L.bd_attn_stage_names.restype = ctypes.c_char_p
     L.bd_attn_stage_names.argtypes = [ci, ci]
     L.bd_attn_workspace_bytes.restype = sz

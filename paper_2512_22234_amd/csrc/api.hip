@@ -115,15 +115,10 @@ int validate_varlen(const int32_t* cu, int n_seqs, int total_L, int max_L, int S
   return BD_ATTN_OK;
 }
 
-// Validation of a decode call; fills the resolved shape.  keys_per_split = 0
-// picks the split length: long enough that a split streams a few hundred KiB,
-// short enough that the longest sequence spreads over many workgroups.
-int validate_decode(int B, int S, int Hq, int Hkv, int D, int C, int max_len, float scale, int dtype,
-                    int keys_per_split, bd::DecodeShape& s) {
-  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || C < 0 || C > (1 << 22) || max_len < 0 ||
-      max_len > C || S > (1 << 22) || keys_per_split < 0 || keys_per_split % bd::DEC_KT != 0)
+// Validation of a decode call; fills the resolved shape.
+int validate_decode(int B, int S, int Hq, int Hkv, int D, int C, float scale, int dtype, bd::DecodeShape& s) {
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || C < 0 || C > (1 << 22) || S > (1 << 22))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
-  if ((size_t)Hq / Hkv * S > (size_t)INT32_MAX / 2) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (D != 64 && D != 128) return BD_ATTN_ERR_UNSUPPORTED;
   if (dtype != BD_ATTN_BF16) return BD_ATTN_ERR_UNSUPPORTED;
@@ -133,18 +128,10 @@ int validate_decode(int B, int S, int Hq, int Hkv, int D, int C, int max_len, fl
   s.Hkv = Hkv;
   s.D = D;
   s.C = C;
-  s.max_len = max_len;
   s.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)D);
-  const size_t items = (size_t)B * Hkv * bd::decode_query_tiles(s);
-  const int nt = bd::decode_key_tiles(s);
-  if (keys_per_split > 0) {
-    s.tps = keys_per_split / bd::DEC_KT;
-  } else {
-    const size_t want = 2048;  // workgroups for the whole call if every sequence were max_len long
-    const size_t t = (items * nt + want - 1) / want;
-    s.tps = (int)(t < 8 ? 8 : t > 64 ? 64 : t);
-  }
-  if (items * bd::decode_splits(s) > (size_t)INT32_MAX) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  // the kernels count key tiles of all items (at most every cache full) in int32
+  const size_t tiles = bd::decode_items(s) * (size_t)(bd::cdiv(C, bd::DEC_KT) + bd::cdiv(S, bd::DEC_KT));
+  if (tiles > (size_t)INT32_MAX / 2) return BD_ATTN_ERR_INVALID_ARGUMENT;
   return BD_ATTN_OK;
 }
 
@@ -356,24 +343,22 @@ int bd_attn_varlen_bwd(const void* dO, const void* Q, const void* K, const void*
   return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, ws_bytes, stream, Marks{nullptr, 0});
 }
 
-size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int max_len, int dtype,
-                                      int keys_per_split) {
+size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int dtype) {
   bd::DecodeShape s;
-  if (validate_decode(B, S, Hq, Hkv, D, capacity, max_len, 0.f, dtype, keys_per_split, s) != BD_ATTN_OK) return 0;
-  return bd::decode_splits(s) > 1 ? align256(bd::decode_partial_floats(s) * 4) : 0;
+  if (validate_decode(B, S, Hq, Hkv, D, capacity, 0.f, dtype, s) != BD_ATTN_OK) return 0;
+  return bd::decode_workspace_bytes(s);
 }
 
 int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, const void* K_new,
                        const void* V_new, const int32_t* cache_lens, int B, int S, int Hq, int Hkv, int D,
-                       int capacity, int max_len, float scale, int dtype, int keys_per_split, void* O, float* LSE,
-                       void* ws, size_t ws_bytes, hipStream_t stream) {
+                       int capacity, float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
   bd::DecodeShape s;
-  const int st = validate_decode(B, S, Hq, Hkv, D, capacity, max_len, scale, dtype, keys_per_split, s);
+  const int st = validate_decode(B, S, Hq, Hkv, D, capacity, scale, dtype, s);
   if (st != BD_ATTN_OK) return st;
-  const size_t need = bd::decode_splits(s) > 1 ? align256(bd::decode_partial_floats(s) * 4) : 0;
+  const size_t need = bd::decode_workspace_bytes(s);
   const bool cache = capacity > 0;
-  if (!Q || !K_new || !V_new || !cache_lens || !O || !LSE || (cache && (!K_cache || !V_cache)) ||
-      (need > 0 && !ws))
+  if (!Q || !K_new || !V_new || !cache_lens || !O || !LSE || !ws || (cache && (!K_cache || !V_cache)))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(Q, 16) || !aligned(K_new, 16) || !aligned(V_new, 16) || !aligned(K_cache, 16) ||
       !aligned(V_cache, 16) || !aligned(cache_lens, 4) || !aligned(O, 16) || !aligned(LSE, 4) || !aligned(ws, 16))
@@ -385,12 +370,11 @@ int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, 
   const Range out[] = {{O, nq * D * 2}, {LSE, nq * 4}, {ws, need}};
   for (const Range& o : out)
     for (const Range& i : in)
-      if (o.p && i.p && overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
-  if (overlap(out[0], out[1]) || (need > 0 && (overlap(out[0], out[2]) || overlap(out[1], out[2]))))
+      if (i.p && overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2]))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   (void)hipGetLastError();
-  float* part = static_cast<float*>(ws);
-  return bd::launch_decode(s, Q, K_cache, V_cache, K_new, V_new, cache_lens, O, LSE, part, stream) == hipSuccess
+  return bd::launch_decode(s, Q, K_cache, V_cache, K_new, V_new, cache_lens, O, LSE, ws, stream) == hipSuccess
              ? BD_ATTN_OK
              : BD_ATTN_ERR_HIP;
 }

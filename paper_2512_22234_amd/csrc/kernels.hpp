@@ -89,36 +89,32 @@ inline size_t dkdv_pair_ints(int B, int Hkv, int L) {
 // (capacity C) and the block's own S keys.
 //   Q, O   : [B][Hq][S][D]      K/V cache : [B][Hkv][C][D]
 //   K/V new: [B][Hkv][S][D]     LSE       : [B][Hq][S] float32
-// The G*S query rows of one KV head are cut into DEC_QT-row tiles and the
-// keys (cache, then block) into DEC_KT-key tiles; a workgroup takes `tps`
-// consecutive key tiles (one split) of one (sequence, KV head, query tile).
-constexpr int DEC_QT = 32, DEC_KT = 32;
+// An item is (sequence, KV head, DEC_QT-row tile of the G*S query rows); its
+// keys (cache, then block) are cut into DEC_KT-key tiles.  The tiles of all
+// items, in item order, are shared out in equal contiguous runs over
+// DEC_WAVES waves (DEC_WAVES / 4 workgroups of four).
+constexpr int DEC_QT = 32, DEC_KT = 32, DEC_WAVES = 1024;
 
 struct DecodeShape {
   int B, S, Hq, Hkv, D;
-  int C;        // cache capacity (rows per sequence and KV head)
-  int max_len;  // bound on every cache length (sizes the grid)
-  int tps;      // key tiles per split
+  int C;  // cache capacity (rows per sequence and KV head)
   float scale;
 };
 
 inline int decode_query_tiles(const DecodeShape& s) { return (s.Hq / s.Hkv * s.S + DEC_QT - 1) / DEC_QT; }
-// Key tiles of the longest sequence.
-inline int decode_key_tiles(const DecodeShape& s) {
-  return (s.max_len + DEC_KT - 1) / DEC_KT + (s.S + DEC_KT - 1) / DEC_KT;
-}
-inline int decode_splits(const DecodeShape& s) { return (decode_key_tiles(s) + s.tps - 1) / s.tps; }
-// float32 elements of one split's partial row: D values, then max and sum
-// (padded to 16 bytes).
+inline size_t decode_items(const DecodeShape& s) { return (size_t)s.B * s.Hkv * decode_query_tiles(s); }
+// float32 elements of one partial row: D values, then max and sum (padded to 16 bytes).
 inline int decode_part_stride(int D) { return D + 4; }
-// Partial results of every split: [item][split][DEC_QT rows][stride].
-inline size_t decode_partial_floats(const DecodeShape& s) {
-  return (size_t)s.B * s.Hkv * decode_query_tiles(s) * decode_splits(s) * DEC_QT * decode_part_stride(s.D);
+// Workspace: per item a 16-byte descriptor, then the partial results of every
+// (wave, item) run: at most DEC_WAVES + items of them, DEC_QT rows each.
+inline size_t decode_desc_bytes(const DecodeShape& s) { return (decode_items(s) * 16 + 255) & ~(size_t)255; }
+inline size_t decode_workspace_bytes(const DecodeShape& s) {
+  return decode_desc_bytes(s) + (DEC_WAVES + decode_items(s)) * DEC_QT * decode_part_stride(s.D) * 4;
 }
 
-// Enqueues the decode kernel and, when the key range is split, the kernel
-// that merges the splits (`part` holds decode_partial_floats floats).
+// Enqueues the decode kernel and the kernel that merges the runs of items
+// shared by several waves.
 hipError_t launch_decode(const DecodeShape& s, const void* Q, const void* Kc, const void* Vc, const void* Kn,
-                         const void* Vn, const int* cache_lens, void* O, float* LSE, float* part, hipStream_t st);
+                         const void* Vn, const int* cache_lens, void* O, float* LSE, void* ws, hipStream_t st);
 
 }  // namespace bd

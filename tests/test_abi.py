@@ -172,36 +172,35 @@ def test_bwd_validation(kw, status):
 
 def test_decode_workspace_bytes():
     f = bd.bd_attn_decode_workspace_bytes
-    # B=64, Hkv=8, one 32-row query tile each (G*S = 16); caches up to 8192
-    # keys: the longest sequence needs more than one split, so partials exist
-    n = f(64, 4, 32, 8, 128, 8192, 8192, 0, 2048)
-    assert n == 64 * 8 * 1 * 5 * 32 * (128 + 4) * 4       # ceil(257 tiles / 64) = 5 splits
-    assert f(64, 4, 32, 8, 128, 8192, 8192, 0, 8192 + 32) == 0   # one split: no partials
-    assert f(2, 4, 4, 2, 64, 100, 0, 0, 0) == 0             # max_len = 0: the block alone
-    assert f(64, 4, 32, 8, 128, 8192, 8192, 0, 0) > 0       # automatic split length
-    for bad in [dict(dtype=1), dict(D=96), dict(Hq=31), dict(kps=48), dict(kps=-32), dict(max_len=101),
-                dict(C=-1), dict(S=0), dict(B=0)]:
-        a = dict(B=2, S=4, Hq=4, Hkv=2, D=64, C=100, max_len=100, dtype=0, kps=0)
+    # B=64, Hkv=8, one 32-row query tile each (G*S = 16): 512 items, a 16-byte
+    # descriptor each, then partial slots for up to 1024 + 512 (wave, item) runs
+    items = 64 * 8
+    assert f(64, 4, 32, 8, 128, 8192, 0) == items * 16 + (1024 + items) * 32 * (128 + 4) * 4
+    assert f(2, 4, 4, 2, 64, 0, 0) > 0                       # no cache: the block alone
+    for bad in [dict(dtype=1), dict(D=96), dict(Hq=31), dict(C=-1), dict(C=(1 << 22) + 1), dict(S=0), dict(B=0)]:
+        a = dict(B=2, S=4, Hq=4, Hkv=2, D=64, C=100, dtype=0)
         a.update(bad)
-        assert f(a["B"], a["S"], a["Hq"], a["Hkv"], a["D"], a["C"], a["max_len"], a["dtype"], a["kps"]) == 0, bad
+        assert f(a["B"], a["S"], a["Hq"], a["Hkv"], a["D"], a["C"], a["dtype"]) == 0, bad
+    # the kernels count key tiles in int32
+    assert f(1 << 16, 4, 64, 64, 128, 1 << 22, 0) == 0
 
 
 def _dec(**kw):
     a = dict(Q=A, Kc=A + SZ, Vc=A + 2 * SZ, Kn=A + 3 * SZ, Vn=A + 4 * SZ, lens=A + 5 * SZ, B=1, S=4, Hq=2,
-             Hkv=1, D=64, C=64, max_len=64, scale=0.0, dtype=0, kps=32, O=A + 6 * SZ, LSE=A + 7 * SZ,
+             Hkv=1, D=64, C=64, scale=0.0, dtype=0, O=A + 6 * SZ, LSE=A + 7 * SZ,
              ws=A + 8 * SZ, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     vp = ctypes.c_void_p
     return _lib.lib().bd_attn_decode_fwd(
         vp(a["Q"]), vp(a["Kc"]), vp(a["Vc"]), vp(a["Kn"]), vp(a["Vn"]), vp(a["lens"]), a["B"], a["S"], a["Hq"],
-        a["Hkv"], a["D"], a["C"], a["max_len"], a["scale"], a["dtype"], a["kps"], vp(a["O"]), vp(a["LSE"]),
+        a["Hkv"], a["D"], a["C"], a["scale"], a["dtype"], vp(a["O"]), vp(a["LSE"]),
         vp(a["ws"]), a["ws_bytes"], vp(a["stream"]))
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(D=96), 2), (dict(dtype=1), 2),
-    (dict(Hq=3, Hkv=2), 1), (dict(B=0), 1), (dict(S=0), 1), (dict(max_len=65), 1), (dict(C=(1 << 22) + 1), 1),
-    (dict(kps=40), 1), (dict(scale=float("inf")), 1),
+    (dict(Hq=3, Hkv=2), 1), (dict(B=0), 1), (dict(S=0), 1), (dict(C=(1 << 22) + 1), 1), (dict(C=-1), 1),
+    (dict(scale=float("inf")), 1),
     (dict(Q=0), 1), (dict(Kn=0), 1), (dict(lens=0), 1), (dict(O=0), 1), (dict(Kc=0), 1), (dict(ws=0), 1),
     (dict(Q=A + 8), 1), (dict(lens=A + 5 * SZ + 2), 1), (dict(LSE=A + 7 * SZ + 2), 1),
     (dict(O=A + 64), 1),                   # output overlaps Q
