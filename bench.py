@@ -221,7 +221,8 @@ def decode_step(steps: int, warmup: int, name: str = "8b_decode"):
     return {"workload": f"{name}: B={B} Hq={Hq} Hkv={Hkv} D={D} S={S}, capacity {C}, cache lengths "
                         f"log-uniform {c['lo']}..{c['hi']} (sum {sum(lens)}), bf16",
             "us_per_call": round(ms * 1e3, 2), "algorithmic_bytes": nbytes, "gbs": round(gbs, 1),
-            "peak_gbs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+            "bound": "hbm", "peak_gbs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "traffic": measured_traffic("decode", "8b"), "traffic_unit": "HBM bytes per launch of the decode kernel"}
 
 
 def main():

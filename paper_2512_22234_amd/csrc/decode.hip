@@ -339,36 +339,38 @@ __global__ __launch_bounds__(256, 1) void dec_kernel(DecParams p, const int* __r
 
 // Merge the runs of each query row of an item held by several waves:
 // O = sum_r 2^(m_r - M) O_r / sum_r 2^(m_r - M) l_r with M = max_r m_r, over
-// the runs of waves first..last that hold tiles.  One thread per (item, row,
-// 4 features).
+// the runs of waves first..last that hold tiles, merged in one pass (the
+// running maximum moves as runs are added, so every run's loads are
+// independent of the others' results).  One thread per (query row, 4
+// features); rows are those of Q, so no thread is spent on padding rows of a
+// query tile.
 template <int D>
-__global__ __launch_bounds__(256) void dec_combine_kernel(DecParams p, int nitems) {
+__global__ __launch_bounds__(256) void dec_combine_kernel(DecParams p) {
   constexpr int TPR = D / 4, PST = D + 4;
   const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const size_t rowid = gid / TPR;  // item * 32 + r
+  const size_t qrow = gid / TPR;  // row of Q: ((b * Hq + h) * S + s)
   const int q4 = (int)(gid % TPR);
-  if (rowid >= (size_t)nitems * DEC_QT) return;
-  const int item = (int)(rowid / DEC_QT), r = (int)(rowid % DEC_QT);
-  const int I = p.Hkv * p.nqt;
-  const int b = item / I, ri = item - b * I;
-  const int hkv = ri / p.nqt, R = (ri - hkv * p.nqt) * DEC_QT + r;
-  if (R >= p.G * p.S) return;
+  const int GS = p.G * p.S;
+  if (qrow >= (size_t)p.B * p.Hkv * GS) return;
+  const int R = (int)(qrow % GS);
+  const size_t bh = qrow / GS;  // b * Hkv + hkv
+  const int item = (int)(bh * p.nqt) + R / DEC_QT, r = R % DEC_QT;
   const int4 d = p.desc[item];
   if (d.y < 0) return;  // written by the decode kernel itself
   const int T = d.z;
-  const size_t qrow = ((size_t)b * p.Hq + (size_t)hkv * p.G) * p.S + R;
-  float M = -INFINITY;
-  for (int gw = d.x; gw <= d.y; ++gw)
-    if (dec_run_start(gw, T) < dec_run_start(gw + 1, T))
-      M = fmaxf(M, p.part[((size_t)(gw + item) * DEC_QT + r) * PST + D]);
-  float Lr = 0.f;
+  float M = -INFINITY, Lr = 0.f;
   f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
   for (int gw = d.x; gw <= d.y; ++gw) {
-    if (dec_run_start(gw, T) == dec_run_start(gw + 1, T)) continue;  // a wave without tiles
     const float* ps = p.part + ((size_t)(gw + item) * DEC_QT + r) * PST;
-    const float a = fast_exp2(ps[D] - M);
-    Lr += a * ps[D + 1];
-    o += a * *reinterpret_cast<const f32x4*>(ps + 4 * q4);
+    const f32x4 ml = *reinterpret_cast<const f32x4*>(ps + D);
+    const f32x4 v = *reinterpret_cast<const f32x4*>(ps + 4 * q4);
+    if (dec_run_start(gw, T) == dec_run_start(gw + 1, T)) continue;  // a wave without tiles wrote nothing
+    const float Mn = fmaxf(M, ml[0]);
+    const float a = fast_exp2(M - Mn), c = fast_exp2(ml[0] - Mn);  // a = 0 for the first run (M = -inf)
+    Lr = Lr * a + ml[1] * c;
+    o = o * a + v * c;
+    M = Mn;
   }
   const float inv = 1.f / Lr;
   st_bf16x4(p.O + qrow * D + 4 * q4, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
@@ -397,12 +399,11 @@ hipError_t launch_decode_d(const DecodeShape& s, const void* Q, const void* Kc, 
   p.C = s.C;
   p.nqt = decode_query_tiles(s);
   p.c = s.scale * LOG2E;
-  const int nitems = (int)decode_items(s);
   hipLaunchKernelGGL(dec_kernel<D>, dim3(DEC_WAVES / 4), dim3(256), 0, st, p, cache_lens);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t threads = (size_t)nitems * DEC_QT * (D / 4);
-  hipLaunchKernelGGL(dec_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, p, nitems);
+  const size_t threads = (size_t)s.B * s.Hq * s.S * (D / 4);
+  hipLaunchKernelGGL(dec_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
