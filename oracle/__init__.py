@@ -1,4 +1,5 @@
-"""Plain fp64 CPU oracle for block-diffusion masked attention.
+"""Plain fp64 CPU oracle for block-diffusion masked attention and for the
+token log-probabilities and objectives that consume its output.
 
 TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
 benchmark's CPU-baseline leg may import this package; the product path
@@ -16,4 +17,10 @@ from .bd_attn_oracle import (  # noqa: F401
     varlen_forward,
     varlen_backward,
     decode_forward,
+)
+from .lce_oracle import (  # noqa: F401
+    lm_head_logprobs,
+    lm_head_backward,
+    masked_ce_objective,
+    dipo_objective,
 )
