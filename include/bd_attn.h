@@ -216,6 +216,61 @@ int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, 
 /* Workspace bytes for bd_attn_decode_fwd; 0 for arguments it would reject. */
 size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int capacity, int dtype);
 
+/*
+ * Token log-probabilities through the LM head, for the training objectives of
+ * blockwise models: the w(t)-weighted cross-entropy over masked positions
+ * (Section 2.1, Eq. 3) and the DiPO clipped surrogate with a KL penalty
+ * (Section 3.2, Eq. 6-7), both functions of log p(target | position) at the
+ * scored positions.  The attention path's output, after the model's last
+ * layers, is the input here.
+ *
+ *   logits[n][v] = sum_d H[n][d] W[v][d]   (never written to memory)
+ *   LSE[n]       = log sum_v exp(logits[n][v])
+ *   logp[n]      = logits[n][targets[n]] - LSE[n]
+ *
+ * H: [N, Dm] bf16 (final hidden states of the scored positions), W: [V, Dm]
+ * bf16 (LM head), both 16-byte aligned; targets: [N] int32, a target outside
+ * [0, V) marks a position that is not scored (logp 0, no gradient).
+ * 1 <= N <= 2^22, 1 <= V <= 2^22, Dm a multiple of 256 up to 2^16.  dtype:
+ * BD_ATTN_BF16 only.  Float32 accumulation throughout.
+ * Ownership, stream order and errors are as for bd_attn_fwd.
+ */
+int bd_lce_fwd(const void* H, const void* W, const int32_t* targets, int N, int V, int Dm, int dtype,
+               float* LSE, float* logp, void* ws, size_t ws_bytes, hipStream_t stream);
+/*
+ * Gradients for a per-position coefficient dlogp[n] = dLoss / dlogp[n]
+ * (from bd_lce_objective, or any loss of the log-probabilities), given the
+ * forward's LSE:
+ *   g[n][v] = dlogp[n] (1[v = targets[n]] - exp(logits[n][v] - LSE[n]))
+ *   dH = g W  ([N, Dm] bf16),   dW = g^T H  ([V, Dm] bf16).
+ * g is recomputed from H and W and kept in the workspace as bf16
+ * ([N, V rounded up to 256]).
+ */
+int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* LSE, const float* dlogp, int N,
+               int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Workspace bytes for bd_lce_fwd (for_bwd = 0) or bd_lce_bwd (for_bwd = 1); 0
+ * for arguments they would reject. */
+size_t bd_lce_workspace_bytes(int N, int V, int Dm, int dtype, int for_bwd);
+
+enum bd_lce_objective_kind { BD_LCE_CE = 0, BD_LCE_DIPO = 1 };
+/*
+ * Per-position objective values and their derivative dlogp = dloss/dlogp
+ * (float32 [N] device arrays; weight carries the per-position factor: the
+ * masked-position indicator times w(t) for Eq. 3, or 1 / (total trajectory
+ * length) for Eq. 7).
+ *   BD_LCE_CE   (Eq. 3):   loss = -weight logp.
+ *   BD_LCE_DIPO (Eq. 6-7): r = exp(logp - logp_old),
+ *                          s = min(r adv, clip(r, 1 - eps, 1 + eps) adv),
+ *                          kl = exp(logp_ref - logp) - (logp_ref - logp) - 1,
+ *                          loss = -weight (s - beta kl).
+ *     With online updates the behaviour policy is the detached current one:
+ *     pass logp itself as logp_old (r = 1).  logp_ref may be NULL when
+ *     beta = 0.  eps, beta >= 0.
+ */
+int bd_lce_objective(const float* logp, const float* logp_old, const float* logp_ref, const float* adv,
+                     const float* weight, int N, int kind, float eps, float beta, float* loss, float* dlogp,
+                     hipStream_t stream);
+
 /* Comma-separated names of the kernels bd_attn_fwd (for_bwd = 0) or
  * bd_attn_bwd (for_bwd = 1) launch for `dtype`, in launch order (static). */
 const char* bd_attn_stage_names(int for_bwd, int dtype);

@@ -23,4 +23,5 @@ from .lce_oracle import (  # noqa: F401
     lm_head_backward,
     masked_ce_objective,
     dipo_objective,
+    lm_head_sampled,
 )

@@ -99,3 +99,33 @@ def dipo_objective(logp, logp_old, logp_ref, adv, weight, eps, beta):
         kl = np.zeros_like(logp)
         dkl = np.zeros_like(logp)
     return -w * (s - beta * kl), -w * (ds - beta * dkl)
+
+
+def lm_head_sampled(H, W, targets, dlogp, rows, vocab_rows, chunk=16384):
+    """The same quantities at a few positions, for shapes whose full logits do
+    not fit in memory: (logp[rows], lse[rows], dH[rows], dW[vocab_rows]).
+    dW[vocab_rows] is exact when dlogp vanishes outside `rows` (it sums over
+    those positions only).  The logits of the chosen rows are computed in
+    vocabulary chunks of `chunk` rows of W (float64), which changes only the
+    memory bound, not the arithmetic of any entry."""
+    rows = np.asarray(rows, dtype=np.int64)
+    vocab_rows = np.asarray(vocab_rows, dtype=np.int64)
+    Hr = _as64(np.asarray(H)[rows])
+    V = W.shape[0]
+    logits = np.empty((len(rows), V))
+    for v0 in range(0, V, chunk):
+        logits[:, v0:v0 + chunk] = Hr @ _as64(np.asarray(W[v0:v0 + chunk])).T
+    m = logits.max(axis=1, keepdims=True)
+    lse = (m + np.log(np.exp(logits - m).sum(axis=1, keepdims=True)))[:, 0]
+    t = np.asarray(targets, dtype=np.int64)[rows]
+    valid = (t >= 0) & (t < V)
+    logp = np.where(valid, logits[np.arange(len(rows)), np.where(valid, t, 0)] - lse, 0.0)
+    c = np.where(valid, _as64(np.asarray(dlogp)[rows]), 0.0)
+    g = -np.exp(logits - lse[:, None])
+    g[np.nonzero(valid)[0], t[valid]] += 1.0
+    g *= c[:, None]
+    dH = np.zeros((len(rows), W.shape[1]))
+    for v0 in range(0, V, chunk):
+        dH += g[:, v0:v0 + chunk] @ _as64(np.asarray(W[v0:v0 + chunk]))
+    dW = g[:, vocab_rows].T @ Hr
+    return logp, lse, dH, dW

@@ -30,6 +30,8 @@ __all__ = [
     "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
     "bd_attn_varlen", "BdAttnVarlenFunction", "bd_attn_varlen_fwd", "bd_attn_varlen_bwd",
     "bd_attn_varlen_workspace_bytes", "bd_attn_decode_fwd", "bd_attn_decode_workspace_bytes",
+    "bd_lce_fwd", "bd_lce_bwd", "bd_lce_workspace_bytes", "bd_lce_objective", "LceFunction", "lm_head_logprobs",
+    "BD_LCE_CE", "BD_LCE_DIPO",
 ]
 
 
@@ -352,3 +354,108 @@ def bd_attn_decode_fwd(q, k_cache, v_cache, k_new, v_new, cache_lens, scale=None
     if stream is not None and workspace is None:
         ws.record_stream(s)
     return o, l_
+
+
+# ---------------------------------------------------------------------------
+# Token log-probabilities through the LM head (Eq. 3 and Eq. 6-7 objectives).
+
+BD_LCE_CE = 0
+BD_LCE_DIPO = 1
+
+
+def bd_lce_workspace_bytes(N, V, Dm, for_bwd, dtype=BD_ATTN_BF16) -> int:
+    return int(lib().bd_lce_workspace_bytes(N, V, Dm, int(dtype), int(for_bwd)))
+
+
+def _lce_shapes(h, w, targets):
+    if h.dim() != 2 or w.dim() != 2 or h.shape[1] != w.shape[1]:
+        raise ValueError("h [N, Dm] and w [V, Dm] expected")
+    N, Dm = h.shape
+    V = w.shape[0]
+    dev = h.device
+    _check("h", h, (N, Dm), torch.bfloat16, dev)
+    _check("w", w, (V, Dm), torch.bfloat16, dev)
+    _check("targets", targets, (N,), torch.int32, dev)
+    return N, V, Dm, dev
+
+
+def bd_lce_fwd(h, w, targets, lse=None, logp=None, workspace=None, stream=None):
+    """Per-position LSE and log p(target) (float32 [N]) of logits h w^T."""
+    N, V, Dm, dev = _lce_shapes(h, w, targets)
+    l_ = torch.empty(N, dtype=torch.float32, device=dev) if lse is None else lse
+    lp = torch.empty(N, dtype=torch.float32, device=dev) if logp is None else logp
+    _check("lse", l_, (N,), torch.float32, dev)
+    _check("logp", lp, (N,), torch.float32, dev)
+    nbytes = bd_lce_workspace_bytes(N, V, Dm, 0)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    st = lib().bd_lce_fwd(_ptr(h), _ptr(w), _ptr(targets), N, V, Dm, BD_ATTN_BF16, _ptr(l_), _ptr(lp), _ptr(ws),
+                          ws.numel(), sh)
+    if st:
+        raise BdAttnError(st, "bd_lce_fwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return l_, lp
+
+
+def bd_lce_bwd(h, w, targets, lse, dlogp, dh=None, dw=None, workspace=None, stream=None):
+    """dH [N, Dm] and dW [V, Dm] (bf16) for dLoss/dlogp = dlogp."""
+    N, V, Dm, dev = _lce_shapes(h, w, targets)
+    _check("lse", lse, (N,), torch.float32, dev)
+    _check("dlogp", dlogp, (N,), torch.float32, dev)
+    dh_ = torch.empty_like(h) if dh is None else dh
+    dw_ = torch.empty_like(w) if dw is None else dw
+    _check("dh", dh_, (N, Dm), torch.bfloat16, dev)
+    _check("dw", dw_, (V, Dm), torch.bfloat16, dev)
+    nbytes = bd_lce_workspace_bytes(N, V, Dm, 1)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
+    s, sh = _stream(dev, stream)
+    st = lib().bd_lce_bwd(_ptr(h), _ptr(w), _ptr(targets), _ptr(lse), _ptr(dlogp), N, V, Dm, BD_ATTN_BF16,
+                          _ptr(dh_), _ptr(dw_), _ptr(ws), ws.numel(), sh)
+    if st:
+        raise BdAttnError(st, "bd_lce_bwd")
+    if stream is not None and workspace is None:
+        ws.record_stream(s)
+    return dh_, dw_
+
+
+def bd_lce_objective(logp, weight, kind=BD_LCE_CE, logp_old=None, logp_ref=None, adv=None, eps=0.2, beta=0.0,
+                     loss=None, dlogp=None, stream=None):
+    """Per-position loss and dloss/dlogp (float32 [N]) of the masked CE (kind
+    BD_LCE_CE) or the DiPO clipped surrogate with KL (kind BD_LCE_DIPO)."""
+    N = logp.numel()
+    dev = logp.device
+    for name, t in (("logp", logp), ("weight", weight), ("logp_old", logp_old), ("logp_ref", logp_ref),
+                    ("adv", adv)):
+        if t is not None:
+            _check(name, t, (N,), torch.float32, dev)
+    lo = torch.empty(N, dtype=torch.float32, device=dev) if loss is None else loss
+    dl = torch.empty(N, dtype=torch.float32, device=dev) if dlogp is None else dlogp
+    opt = lambda t: ctypes.c_void_p(None) if t is None else _ptr(t)  # noqa: E731
+    _, sh = _stream(dev, stream)
+    st = lib().bd_lce_objective(_ptr(logp), opt(logp_old), opt(logp_ref), opt(adv), _ptr(weight), N, int(kind),
+                                float(eps), float(beta), _ptr(lo), _ptr(dl), sh)
+    if st:
+        raise BdAttnError(st, "bd_lce_objective")
+    return lo, dl
+
+
+class LceFunction(torch.autograd.Function):
+    """log p(target) through the LM head; differentiable in h and w."""
+
+    @staticmethod
+    def forward(ctx, h, w, targets):
+        lse, logp = bd_lce_fwd(h, w, targets)
+        ctx.save_for_backward(h, w, targets, lse)
+        return logp
+
+    @staticmethod
+    def backward(ctx, dlogp):
+        h, w, targets, lse = ctx.saved_tensors
+        dh, dw = bd_lce_bwd(h, w, targets, lse, dlogp.contiguous().float())
+        return dh, dw, None
+
+
+def lm_head_logprobs(h, w, targets):
+    """Differentiable per-position log p(target) [N] float32 (targets outside [0, V): 0)."""
+    return LceFunction.apply(h, w, targets)

@@ -51,6 +51,14 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_decode_fwd.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci, vp, vp, vp, sz, vp]
     L.bd_attn_decode_workspace_bytes.restype = sz
     L.bd_attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci]
+    L.bd_lce_fwd.restype = ci
+    L.bd_lce_fwd.argtypes = [vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, sz, vp]
+    L.bd_lce_bwd.restype = ci
+    L.bd_lce_bwd.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, sz, vp]
+    L.bd_lce_workspace_bytes.restype = sz
+    L.bd_lce_workspace_bytes.argtypes = [ci, ci, ci, ci, ci]
+    L.bd_lce_objective.restype = ci
+    L.bd_lce_objective.argtypes = [vp, vp, vp, vp, vp, ci, ci, cf, cf, vp, vp, vp]
     L.bd_attn_stage_names.restype = ctypes.c_char_p
     L.bd_attn_stage_names.argtypes = [ci, ci]
     L.bd_attn_workspace_bytes.restype = sz

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libbd_attn.so")
-SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "decode.hip", "aux.hip"]
+SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "decode.hip", "lce.hip", "aux.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -135,6 +135,19 @@ int validate_decode(int B, int S, int Hq, int Hkv, int D, int C, float scale, in
   return BD_ATTN_OK;
 }
 
+// Validation of the LM-head calls; fills the shape.
+int validate_lce(int N, int V, int Dm, int dtype, bd::LceShape& s) {
+  // buffer offsets of one 256-row operand tile stay below 2^32 bytes for
+  // rows of up to 2^22 elements
+  if (N < 1 || V < 1 || Dm < 256 || Dm % 256 != 0 || N > (1 << 22) || V > (1 << 22) || Dm > (1 << 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (dtype != BD_ATTN_BF16) return BD_ATTN_ERR_UNSUPPORTED;
+  s.N = N;
+  s.V = V;
+  s.Dm = Dm;
+  return BD_ATTN_OK;
+}
+
 #define BD_TRY(expr)                                    \
   do {                                                  \
     if ((expr) != hipSuccess) return BD_ATTN_ERR_HIP;   \
@@ -375,6 +388,82 @@ int bd_attn_decode_fwd(const void* Q, const void* K_cache, const void* V_cache, 
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   (void)hipGetLastError();
   return bd::launch_decode(s, Q, K_cache, V_cache, K_new, V_new, cache_lens, O, LSE, ws, stream) == hipSuccess
+             ? BD_ATTN_OK
+             : BD_ATTN_ERR_HIP;
+}
+
+size_t bd_lce_workspace_bytes(int N, int V, int Dm, int dtype, int for_bwd) {
+  bd::LceShape s;
+  if (validate_lce(N, V, Dm, dtype, s) != BD_ATTN_OK) return 0;
+  return for_bwd ? bd::lce_bwd_workspace_bytes(s) : bd::lce_fwd_workspace_bytes(s);
+}
+
+int bd_lce_fwd(const void* H, const void* W, const int32_t* targets, int N, int V, int Dm, int dtype, float* lse,
+               float* logp, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd::LceShape s;
+  const int st = validate_lce(N, V, Dm, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  if (!H || !W || !targets || !lse || !logp || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!aligned(H, 16) || !aligned(W, 16) || !aligned(targets, 4) || !aligned(lse, 4) || !aligned(logp, 4) ||
+      !aligned(ws, 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const size_t need = bd::lce_fwd_workspace_bytes(s);
+  if (ws_bytes < need) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
+  const Range in[] = {{H, (size_t)N * Dm * 2}, {W, (size_t)V * Dm * 2}, {targets, (size_t)N * 4}};
+  const Range out[] = {{lse, (size_t)N * 4}, {logp, (size_t)N * 4}, {ws, need}};
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2])) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  (void)hipGetLastError();
+  return bd::launch_lce_fwd(s, H, W, targets, lse, logp, ws, stream) == hipSuccess ? BD_ATTN_OK : BD_ATTN_ERR_HIP;
+}
+
+int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* lse, const float* dlogp, int N,
+               int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd::LceShape s;
+  const int st = validate_lce(N, V, Dm, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  if (!H || !W || !targets || !lse || !dlogp || !dH || !dW || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!aligned(H, 16) || !aligned(W, 16) || !aligned(targets, 4) || !aligned(lse, 4) || !aligned(dlogp, 4) ||
+      !aligned(dH, 16) || !aligned(dW, 16) || !aligned(ws, 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const size_t need = bd::lce_bwd_workspace_bytes(s);
+  if (ws_bytes < need) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
+  const Range in[] = {{H, (size_t)N * Dm * 2}, {W, (size_t)V * Dm * 2}, {targets, (size_t)N * 4},
+                      {lse, (size_t)N * 4}, {dlogp, (size_t)N * 4}};
+  const Range out[] = {{dH, (size_t)N * Dm * 2}, {dW, (size_t)V * Dm * 2}, {ws, need}};
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2])) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  (void)hipGetLastError();
+  return bd::launch_lce_bwd(s, H, W, targets, lse, dlogp, dH, dW, ws, stream) == hipSuccess ? BD_ATTN_OK
+                                                                                          : BD_ATTN_ERR_HIP;
+}
+
+int bd_lce_objective(const float* logp, const float* logp_old, const float* logp_ref, const float* adv,
+                     const float* weight, int N, int kind, float eps, float beta, float* loss, float* dlogp,
+                     hipStream_t stream) {
+  if (N < 1 || (kind != BD_LCE_CE && kind != BD_LCE_DIPO)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (std::isnan(eps) || std::isinf(eps) || eps < 0.f || std::isnan(beta) || std::isinf(beta) || beta < 0.f)
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!logp || !weight || !loss || !dlogp) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (kind == BD_LCE_DIPO && (!logp_old || !adv || (beta != 0.f && !logp_ref))) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const float* ptrs[] = {logp, logp_old, logp_ref, adv, weight, loss, dlogp};
+  for (const float* q : ptrs)
+    if (!aligned(q, 4)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  const size_t nb = (size_t)N * 4;
+  const Range in[] = {{logp, nb}, {logp_old, logp_old ? nb : 0}, {logp_ref, logp_ref ? nb : 0},
+                      {adv, adv ? nb : 0}, {weight, nb}};
+  const Range out[] = {{loss, nb}, {dlogp, nb}};
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (i.p && overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (overlap(out[0], out[1])) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  (void)hipGetLastError();
+  return bd::launch_lce_objective(N, kind, eps, beta, logp, logp_old, logp_ref, adv, weight, loss, dlogp, stream) ==
+                 hipSuccess
              ? BD_ATTN_OK
              : BD_ATTN_ERR_HIP;
 }

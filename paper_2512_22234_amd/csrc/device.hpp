@@ -62,6 +62,10 @@ template <> __host__ __device__ inline int chunk_swizzle<128>(int r) {
 template <> __host__ __device__ inline int chunk_swizzle<64>(int r) {
   return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
 }
+// 64-byte rows (GEMM k-chunks of 32): four rows share a 256-byte bank cycle,
+// so 16 consecutive rows at one 16-byte column land on 16 distinct bank
+// groups when the chunk moves with row / 4.
+template <> __host__ __device__ inline int chunk_swizzle<32>(int r) { return (r >> 2) & 3; }
 // Element index of (row, col) in a swizzled tile; col % 8 stays in place.
 template <int D> __host__ __device__ inline int tile_idx(int row, int col) {
   return row * D + ((((col >> 3) ^ chunk_swizzle<D>(row)) << 3) | (col & 7));
@@ -113,6 +117,26 @@ struct LdsOperands {
     constexpr int HI = (D / 8 - 1) & ~3;
     tr_rel0 = (uint32_t)(r0 * 2 * D + 16 * (f0 & HI) + 16 * (x ^ (f0 & 3)) + 8 * (j & 1));
     tr_rel1 = (uint32_t)((r0 + 8) * 2 * D + 16 * (f1 & HI) + 16 * (x ^ (f1 & 3)) + 8 * (j & 1));
+  }
+};
+
+// Transposing operand reads in linear k order, for products whose other
+// operand is also read from LDS: lane (l32, g) gets X[row0 + 8g + e][col0 + l32],
+// e = 0..7 -- the slot order of a row-slice read (k = 8g + e), so a
+// transposed tile can meet a row-major one in one MFMA.  Same conflict-free
+// pattern as LdsOperands' reads (four consecutive rows of 32 bytes per group
+// of 16 lanes).  Tile offsets must be multiples of 256 bytes.
+template <int D>
+struct LdsLinearTr {
+  uint32_t rel0, rel1;  // byte offsets of rows 8g + (lane%16)/4 and 8g + 4 + (lane%16)/4
+  __device__ explicit LdsLinearTr(int lane) {
+    const int h = lane >> 4, j = lane & 15;
+    const int x = 2 * (h & 1) + ((j >> 1) & 1);
+    const int r0 = 8 * (h >> 1) + (j >> 2);
+    const int f0 = chunk_swizzle<D>(r0), f1 = chunk_swizzle<D>(r0 + 4);
+    constexpr int HI = (D / 8 - 1) & ~3;
+    rel0 = (uint32_t)(r0 * 2 * D + 16 * (f0 & HI) + 16 * (x ^ (f0 & 3)) + 8 * (j & 1));
+    rel1 = (uint32_t)((r0 + 4) * 2 * D + 16 * (f1 & HI) + 16 * (x ^ (f1 & 3)) + 8 * (j & 1));
   }
 };
 

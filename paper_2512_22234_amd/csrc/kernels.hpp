@@ -117,4 +117,29 @@ inline size_t decode_workspace_bytes(const DecodeShape& s) {
 hipError_t launch_decode(const DecodeShape& s, const void* Q, const void* Kc, const void* Vc, const void* Kn,
                          const void* Vn, const int* cache_lens, void* O, float* LSE, void* ws, hipStream_t st);
 
+// Token log-probabilities through the LM head (H [N][Dm] x W [V][Dm]),
+// fused with their softmax.  Dm is a multiple of 256.
+constexpr int LCE_BK = 32;  // k per GEMM chunk
+struct LceShape {
+  int N, V, Dm;
+};
+inline int lce_vocab_tiles(const LceShape& s) { return (s.V + 255) / 256; }
+inline size_t lce_align(size_t x) { return (x + 255) & ~(size_t)255; }
+// Forward workspace: per (token, vocabulary tile) the partial (max, sum).
+inline size_t lce_fwd_part_offset(const LceShape&) { return 0; }
+inline size_t lce_fwd_workspace_bytes(const LceShape& s) { return lce_align((size_t)s.N * lce_vocab_tiles(s) * 8); }
+// Backward workspace: g = coef (onehot - softmax) as bf16 [N][V rounded up to 256].
+inline size_t lce_bwd_g_offset(const LceShape&) { return 0; }
+inline size_t lce_bwd_workspace_bytes(const LceShape& s) {
+  return lce_align((size_t)s.N * lce_vocab_tiles(s) * 256 * 2);
+}
+
+hipError_t launch_lce_fwd(const LceShape& s, const void* H, const void* W, const int* targets, float* lse,
+                          float* logp, void* ws, hipStream_t st);
+hipError_t launch_lce_bwd(const LceShape& s, const void* H, const void* W, const int* targets, const float* lse,
+                          const float* coef, void* dH, void* dW, void* ws, hipStream_t st);
+hipError_t launch_lce_objective(int N, int kind, float eps, float beta, const float* logp, const float* logp_old,
+                                const float* logp_ref, const float* adv, const float* weight, float* loss,
+                                float* dlogp, hipStream_t st);
+
 }  // namespace bd

@@ -182,3 +182,30 @@ def make_decode_inputs(B: int, Hq: int, Hkv: int, D: int, S: int, capacity: int,
 DECODE_WORKLOADS = {
     "8b_decode": dict(B=64, Hq=32, Hkv=8, D=128, S=4, capacity=8192, lo=512, hi=8192, seed=9),
 }
+
+
+# ---------------------------------------------------------------------------
+# Token log-probabilities through the LM head: the positions scored by the
+# objectives of Eq. 3 and Eq. 6-7 (the noisy positions of a training batch).
+
+def make_lce_inputs(N: int, V: int, Dm: int, seed: int, logit_std: float = 3.0, device: str = "cpu"):
+    """bf16 H [N, Dm] ~ N(0, 1) (normalised final hidden states) and W [V, Dm] ~
+    N(0, logit_std^2 / Dm) (so the logits have standard deviation logit_std),
+    drawn in that order from a generator seeded with `seed` on `device`, and
+    int32 targets uniform in [0, V) from a CPU generator with the same seed."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    h = torch.randn((N, Dm), generator=g, device=device).to(torch.bfloat16)
+    w = (torch.randn((V, Dm), generator=g, device=device) * (logit_std / Dm ** 0.5)).to(torch.bfloat16)
+    gc = torch.Generator(device="cpu")
+    gc.manual_seed(seed)
+    t = torch.randint(0, V, (N,), generator=gc, dtype=torch.int64).to(torch.int32).to(device)
+    return h, w, t
+
+
+# The LM head of the 8B model (hidden 4096; a Qwen3-family vocabulary of
+# 151,936 entries, the base of SDAR-8B) over the 4096 noisy positions of the
+# 8B training batch (two sequences of 2048 tokens).
+LCE_WORKLOADS = {
+    "8b_lm_head": dict(N=4096, V=151936, Dm=4096, seed=10),
+}

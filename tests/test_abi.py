@@ -210,3 +210,71 @@ def _dec(**kw):
 ])
 def test_decode_validation(kw, status):
     assert _dec(**kw) == status
+
+
+def test_lce_workspace_bytes():
+    f = bd.bd_lce_workspace_bytes
+    # forward: a (max, sum) pair per position and vocabulary tile of 256
+    assert f(4096, 151936, 4096, 0) == 4096 * 594 * 8
+    # backward: g as bf16 [N][V rounded up to 256]
+    assert f(4096, 151936, 4096, 1) == 4096 * 594 * 256 * 2
+    for bad in [dict(N=0), dict(V=0), dict(Dm=128), dict(Dm=300), dict(dtype=1), dict(N=(1 << 22) + 1),
+                dict(V=(1 << 22) + 1), dict(Dm=1 << 17)]:
+        a = dict(N=8, V=300, Dm=256, dtype=0)
+        a.update(bad)
+        assert f(a["N"], a["V"], a["Dm"], 0, a["dtype"]) == 0, bad
+
+
+def _lce_fwd(**kw):
+    a = dict(H=A, W=A + SZ, t=A + 2 * SZ, N=8, V=300, Dm=256, dtype=0, lse=A + 3 * SZ, logp=A + 4 * SZ,
+             ws=A + 5 * SZ, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    vp = ctypes.c_void_p
+    return _lib.lib().bd_lce_fwd(vp(a["H"]), vp(a["W"]), vp(a["t"]), a["N"], a["V"], a["Dm"], a["dtype"],
+                                 vp(a["lse"]), vp(a["logp"]), vp(a["ws"]), a["ws_bytes"], vp(a["stream"]))
+
+
+def _lce_bwd(**kw):
+    a = dict(H=A, W=A + SZ, t=A + 2 * SZ, lse=A + 3 * SZ, dl=A + 4 * SZ, N=8, V=300, Dm=256, dtype=0,
+             dH=A + 5 * SZ, dW=A + 6 * SZ, ws=A + 7 * SZ, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    vp = ctypes.c_void_p
+    return _lib.lib().bd_lce_bwd(vp(a["H"]), vp(a["W"]), vp(a["t"]), vp(a["lse"]), vp(a["dl"]), a["N"], a["V"],
+                                 a["Dm"], a["dtype"], vp(a["dH"]), vp(a["dW"]), vp(a["ws"]), a["ws_bytes"],
+                                 vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=1), 2), (dict(N=0), 1), (dict(Dm=384), 1), (dict(H=0), 1), (dict(t=0), 1), (dict(ws=0), 1),
+    (dict(H=A + 8), 1), (dict(lse=A + 3 * SZ + 2), 1),
+    (dict(logp=A + 16), 1),                # output overlaps H
+    (dict(ws=A + 3 * SZ + 16), 1),         # workspace overlaps LSE
+    (dict(ws_bytes=64), 3),
+])
+def test_lce_fwd_validation(kw, status):
+    assert _lce_fwd(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=1), 2), (dict(V=0), 1), (dict(dl=0), 1), (dict(dW=0), 1), (dict(dH=A + 5 * SZ + 4), 1),
+    (dict(dW=A + SZ + 64), 1),             # dW overlaps W
+    (dict(dH=A + 6 * SZ), 1),              # dH overlaps dW
+    (dict(ws_bytes=1000), 3),
+])
+def test_lce_bwd_validation(kw, status):
+    assert _lce_bwd(**kw) == status
+
+
+@pytest.mark.parametrize("kind,eps,beta,old,adv,ref,status", [
+    (2, 0.2, 0.0, 1, 1, 1, 1),             # unknown objective
+    (1, 0.2, 0.0, 0, 1, 0, 1),             # DiPO without logp_old
+    (1, 0.2, 0.1, 1, 1, 0, 1),             # KL without the reference
+    (1, -0.1, 0.0, 1, 1, 0, 1),            # negative clip range
+    (1, 0.2, float("nan"), 1, 1, 1, 1),
+])
+def test_lce_objective_validation(kind, eps, beta, old, adv, ref, status):
+    vp = ctypes.c_void_p
+    p = lambda i, on=1: vp(A + i * SZ if on else 0)  # noqa: E731
+    st = _lib.lib().bd_lce_objective(p(0), p(1, old), p(2, ref), p(3, adv), p(4), 8, kind, eps, beta, p(5), p(6),
+                                     vp(None))
+    assert st == status

@@ -168,3 +168,19 @@ def test_dipo_kl_estimator_properties_and_finite_differences():
     away = np.abs(r - 0.8) > 1e-3
     away &= np.abs(r - 1.2) > 1e-3
     np.testing.assert_allclose(((lp_p - lp_m) / (2 * h))[away], dl[away], rtol=1e-6, atol=1e-8)
+
+
+def test_sampled_matches_full_evaluation():
+    H, W, t = _case(9, 70, 6, 13)
+    t[4] = -1
+    rows = [1, 4, 7]
+    c = np.zeros(9)
+    c[rows] = [0.5, 2.0, -1.5]
+    logp, lse = oracle.lm_head_logprobs(H, W, t)
+    dH, dW = oracle.lm_head_backward(H, W, t, c)
+    vr = [0, 5, 33, 69]
+    slp, slse, sdH, sdW = oracle.lm_head_sampled(H, W, t, c, rows, vr, chunk=16)
+    np.testing.assert_allclose(slp, logp[rows], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(slse, lse[rows], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(sdH, dH[rows], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(sdW, dW[vr], rtol=0, atol=1e-12)
