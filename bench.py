@@ -21,6 +21,11 @@ cpu_baseline: the fp64 oracle (test infrastructure) timed on the host cores on
 packed:  the same step over packed sequences of mixed lengths (the same heads,
          4096 tokens per copy in all) through the varlen calls, reported
          beside the headline (not part of `value`).
+lce:     token log-probabilities through the 8B LM head (4096 scored positions,
+         151,936 vocabulary rows, hidden 4096): forward (GEMM with fused
+         softmax statistics), the Eq. 7 objective, backward (recomputed
+         logits -> g, dH = g W, dW = g^T H); GEMM FLOPs over the event-timed
+         duration against the bf16 dense peak (not part of `value`).
 decode:  one block-decoding call over a KV cache (64 rollouts of the 8B
          shape, caches of 512..8192 tokens, blocks of 4): HBM bytes the call
          must move (cached K/V rows up to each length, the block's K/V, Q, O,
@@ -225,6 +230,65 @@ def decode_step(steps: int, warmup: int, name: str = "8b_decode"):
             "traffic": measured_traffic("decode", "8b"), "traffic_unit": "HBM bytes per launch of the decode kernel"}
 
 
+def lce_step(steps: int, warmup: int, name: str = "8b_lm_head"):
+    """bd_lce_fwd + bd_lce_objective + bd_lce_bwd over the 8B LM head."""
+    import torch
+    import paper_2512_22234_amd as bd
+    from paper_2512_22234_amd.workloads import LCE_WORKLOADS, make_lce_inputs
+    c = LCE_WORKLOADS[name]
+    N, V, Dm = c["N"], c["V"], c["Dm"]
+    h, w, t = make_lce_inputs(N, V, Dm, seed=c["seed"], device="cuda")
+    dev = h.device
+    lse, logp = torch.empty(N, device=dev), torch.empty(N, device=dev)
+    adv = torch.randn(N, device=dev, generator=torch.Generator(device=dev).manual_seed(1))
+    wgt = torch.full((N,), 1.0 / N, device=dev)
+    loss, dlogp = torch.empty(N, device=dev), torch.empty(N, device=dev)
+    dh, dw = torch.empty_like(h), torch.empty_like(w)
+    wsf = torch.empty(bd.bd_lce_workspace_bytes(N, V, Dm, 0), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(bd.bd_lce_workspace_bytes(N, V, Dm, 1), dtype=torch.uint8, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+
+    def step(timed=False):
+        if timed:
+            ev[0].record()
+        bd.bd_lce_fwd(h, w, t, lse=lse, logp=logp, workspace=wsf)
+        if timed:
+            ev[1].record()
+        # Eq. 7: online update, the behaviour policy is the detached current one
+        bd.bd_lce_objective(logp, wgt, bd.BD_LCE_DIPO, logp_old=logp, adv=adv, eps=0.2, beta=0.0, loss=loss,
+                            dlogp=dlogp)
+        if timed:
+            ev[2].record()
+        bd.bd_lce_bwd(h, w, t, lse, dlogp, dh=dh, dw=dw, workspace=wsb)
+        if timed:
+            ev[3].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    tf = to = tb = 0.0
+    for _ in range(steps):
+        step(True)
+        torch.cuda.synchronize()
+        tf += ev[0].elapsed_time(ev[1])
+        to += ev[1].elapsed_time(ev[2])
+        tb += ev[2].elapsed_time(ev[3])
+    tf, to, tb = tf / steps, to / steps, tb / steps
+    gemm = 2.0 * N * V * Dm
+    fwd_tf = gemm / (tf * 1e-3) / 1e12
+    bwd_tf = 3 * gemm / (tb * 1e-3) / 1e12   # executed: recomputed logits, dH, dW
+    step_tf = 3 * gemm / ((tf + to + tb) * 1e-3) / 1e12  # useful: logits, dH, dW
+    log(f"[bench] lce {name}: fwd {tf:.3f} ms ({fwd_tf:.0f} TFLOP/s), objective {to * 1e3:.1f} us, "
+        f"bwd {tb:.3f} ms ({bwd_tf:.0f} TFLOP/s executed)")
+    return {"workload": f"{name}: N={N} scored positions, V={V}, Dm={Dm}, bf16 H ~ N(0,1), W ~ N(0, 9/Dm), "
+                        f"DiPO objective with online ratio",
+            "fwd_ms": round(tf, 4), "objective_ms": round(to, 4), "bwd_ms": round(tb, 4),
+            "step_ms": round(tf + to + tb, 4),
+            "tflops_useful": round(step_tf, 1), "fwd_tflops": round(fwd_tf, 1), "bwd_tflops_executed": round(bwd_tf, 1),
+            "bound": "mfma", "peak_tflops": PEAK_BF16_TFLOPS, "frac_fwd": round(fwd_tf / PEAK_BF16_TFLOPS, 4),
+            "frac_bwd_executed": round(bwd_tf / PEAK_BF16_TFLOPS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -234,6 +298,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-packed", action="store_true", help="skip the packed-sequence measurement")
     ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
+    ap.add_argument("--no-lce", action="store_true", help="skip the LM-head log-probability measurement")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time to spend")
     ap.add_argument("--cpu-max-groups", type=int, default=4)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -333,6 +398,7 @@ def main():
 
     packed = None if args.no_packed else packed_step(args.steps, args.warmup)
     decode = None if args.no_decode else decode_step(args.steps, args.warmup)
+    lce = None if args.no_lce else lce_step(min(args.steps, 10), min(args.warmup, 3))
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -366,6 +432,7 @@ def main():
         "kernels": kernels,
         "packed": packed,
         "decode": decode,
+        "lce": lce,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
