@@ -247,11 +247,12 @@ def lce_step(steps: int, warmup: int, name: str = "8b_lm_head"):
     wsf = torch.empty(bd.bd_lce_workspace_bytes(N, V, Dm, 0), dtype=torch.uint8, device=dev)
     wsb = torch.empty(bd.bd_lce_workspace_bytes(N, V, Dm, 1), dtype=torch.uint8, device=dev)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    keep = None
 
     def step(timed=False):
         if timed:
             ev[0].record()
-        bd.bd_lce_fwd(h, w, t, lse=lse, logp=logp, workspace=wsf)
+        bd.bd_lce_fwd(h, w, t, lse=lse, logp=logp, workspace=wsf, logits=keep)
         if timed:
             ev[1].record()
         # Eq. 7: online update, the behaviour policy is the detached current one
@@ -259,34 +260,45 @@ def lce_step(steps: int, warmup: int, name: str = "8b_lm_head"):
                             dlogp=dlogp)
         if timed:
             ev[2].record()
-        bd.bd_lce_bwd(h, w, t, lse, dlogp, dh=dh, dw=dw, workspace=wsb)
+        bd.bd_lce_bwd(h, w, t, lse, dlogp, dh=dh, dw=dw, workspace=wsb, logits=keep)
         if timed:
             ev[3].record()
 
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    tf = to = tb = 0.0
-    for _ in range(steps):
-        step(True)
+    def measure():
+        for _ in range(warmup):
+            step()
         torch.cuda.synchronize()
-        tf += ev[0].elapsed_time(ev[1])
-        to += ev[1].elapsed_time(ev[2])
-        tb += ev[2].elapsed_time(ev[3])
-    tf, to, tb = tf / steps, to / steps, tb / steps
+        tf = to = tb = 0.0
+        for _ in range(steps):
+            step(True)
+            torch.cuda.synchronize()
+            tf += ev[0].elapsed_time(ev[1])
+            to += ev[1].elapsed_time(ev[2])
+            tb += ev[2].elapsed_time(ev[3])
+        return tf / steps, to / steps, tb / steps
+
+    tf, to, tb = measure()
+    # the same step keeping the forward's logits (float32 [N][V rounded up]) for the backward
+    keep = torch.empty(bd.bd_lce_logits_bytes(N, V, Dm) // 4, dtype=torch.float32, device=dev)
+    kf, ko, kb = measure()
+    keep = None
     gemm = 2.0 * N * V * Dm
     fwd_tf = gemm / (tf * 1e-3) / 1e12
     bwd_tf = 3 * gemm / (tb * 1e-3) / 1e12   # executed: recomputed logits, dH, dW
     step_tf = 3 * gemm / ((tf + to + tb) * 1e-3) / 1e12  # useful: logits, dH, dW
     log(f"[bench] lce {name}: fwd {tf:.3f} ms ({fwd_tf:.0f} TFLOP/s), objective {to * 1e3:.1f} us, "
-        f"bwd {tb:.3f} ms ({bwd_tf:.0f} TFLOP/s executed)")
+        f"bwd {tb:.3f} ms ({bwd_tf:.0f} TFLOP/s executed); keeping the logits: fwd {kf:.3f} ms, bwd {kb:.3f} ms, "
+        f"step {kf + ko + kb:.3f} ms ({3 * gemm / ((kf + ko + kb) * 1e-3) / 1e12:.0f} TFLOP/s)")
     return {"workload": f"{name}: N={N} scored positions, V={V}, Dm={Dm}, bf16 H ~ N(0,1), W ~ N(0, 9/Dm), "
                         f"DiPO objective with online ratio",
             "fwd_ms": round(tf, 4), "objective_ms": round(to, 4), "bwd_ms": round(tb, 4),
             "step_ms": round(tf + to + tb, 4),
             "tflops_useful": round(step_tf, 1), "fwd_tflops": round(fwd_tf, 1), "bwd_tflops_executed": round(bwd_tf, 1),
             "bound": "mfma", "peak_tflops": PEAK_BF16_TFLOPS, "frac_fwd": round(fwd_tf / PEAK_BF16_TFLOPS, 4),
-            "frac_bwd_executed": round(bwd_tf / PEAK_BF16_TFLOPS, 4)}
+            "frac_bwd_executed": round(bwd_tf / PEAK_BF16_TFLOPS, 4),
+            "kept_logits": {"fwd_ms": round(kf, 4), "bwd_ms": round(kb, 4), "step_ms": round(kf + ko + kb, 4),
+                            "tflops_useful": round(3 * gemm / ((kf + ko + kb) * 1e-3) / 1e12, 1),
+                            "logits_bytes": bd.bd_lce_logits_bytes(N, V, Dm)}}
 
 
 def main():

@@ -236,21 +236,30 @@ size_t bd_attn_decode_workspace_bytes(int B, int S, int Hq, int Hkv, int D, int 
  * Ownership, stream order and errors are as for bd_attn_fwd.
  */
 int bd_lce_fwd(const void* H, const void* W, const int32_t* targets, int N, int V, int Dm, int dtype,
-               float* LSE, float* logp, void* ws, size_t ws_bytes, hipStream_t stream);
+               float* LSE, float* logp, float* logits, void* ws, size_t ws_bytes, hipStream_t stream);
 /*
+ * logits (optional, may be NULL): a float32 [N, V rounded up to 256] buffer
+ * (bd_lce_logits_bytes, 16-byte aligned) that receives a copy of the logits
+ * for bd_lce_bwd, which then skips recomputing them.  Without it the logits
+ * exist only tile by tile on chip.
+ *
  * Gradients for a per-position coefficient dlogp[n] = dLoss / dlogp[n]
  * (from bd_lce_objective, or any loss of the log-probabilities), given the
  * forward's LSE:
  *   g[n][v] = dlogp[n] (1[v = targets[n]] - exp(logits[n][v] - LSE[n]))
  *   dH = g W  ([N, Dm] bf16),   dW = g^T H  ([V, Dm] bf16).
- * g is recomputed from H and W and kept in the workspace as bf16
- * ([N, V rounded up to 256]).
+ * g is formed from the logits kept by bd_lce_fwd when `logits` is not NULL,
+ * else recomputed from H and W (one more GEMM), and held in the workspace as
+ * bf16 ([N, V rounded up to 256]).
  */
-int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* LSE, const float* dlogp, int N,
-               int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes, hipStream_t stream);
+int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* LSE, const float* dlogp,
+               const float* logits, int N, int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes,
+               hipStream_t stream);
 /* Workspace bytes for bd_lce_fwd (for_bwd = 0) or bd_lce_bwd (for_bwd = 1); 0
  * for arguments they would reject. */
 size_t bd_lce_workspace_bytes(int N, int V, int Dm, int dtype, int for_bwd);
+/* Bytes of the optional kept-logits buffer; 0 for rejected arguments. */
+size_t bd_lce_logits_bytes(int N, int V, int Dm, int dtype);
 
 enum bd_lce_objective_kind { BD_LCE_CE = 0, BD_LCE_DIPO = 1 };
 /*

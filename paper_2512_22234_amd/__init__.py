@@ -30,7 +30,7 @@ __all__ = [
     "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
     "bd_attn_varlen", "BdAttnVarlenFunction", "bd_attn_varlen_fwd", "bd_attn_varlen_bwd",
     "bd_attn_varlen_workspace_bytes", "bd_attn_decode_fwd", "bd_attn_decode_workspace_bytes",
-    "bd_lce_fwd", "bd_lce_bwd", "bd_lce_workspace_bytes", "bd_lce_objective", "LceFunction", "lm_head_logprobs",
+    "bd_lce_fwd", "bd_lce_bwd", "bd_lce_workspace_bytes", "bd_lce_logits_bytes", "bd_lce_objective", "LceFunction", "lm_head_logprobs",
     "BD_LCE_CE", "BD_LCE_DIPO",
 ]
 
@@ -379,9 +379,18 @@ def _lce_shapes(h, w, targets):
     return N, V, Dm, dev
 
 
-def bd_lce_fwd(h, w, targets, lse=None, logp=None, workspace=None, stream=None):
-    """Per-position LSE and log p(target) (float32 [N]) of logits h w^T."""
+def bd_lce_logits_bytes(N, V, Dm, dtype=BD_ATTN_BF16) -> int:
+    return int(lib().bd_lce_logits_bytes(N, V, Dm, int(dtype)))
+
+
+def bd_lce_fwd(h, w, targets, lse=None, logp=None, workspace=None, stream=None, logits=None):
+    """Per-position LSE and log p(target) (float32 [N]) of logits h w^T.
+    logits: optional float32 tensor of bd_lce_logits_bytes bytes that receives
+    the logits for bd_lce_bwd."""
     N, V, Dm, dev = _lce_shapes(h, w, targets)
+    if logits is not None and (logits.dtype != torch.float32 or logits.numel() * 4 < bd_lce_logits_bytes(N, V, Dm)
+                               or not logits.is_contiguous() or logits.device != dev):
+        raise ValueError("logits: a contiguous float32 buffer of bd_lce_logits_bytes bytes on the device expected")
     l_ = torch.empty(N, dtype=torch.float32, device=dev) if lse is None else lse
     lp = torch.empty(N, dtype=torch.float32, device=dev) if logp is None else logp
     _check("lse", l_, (N,), torch.float32, dev)
@@ -389,7 +398,8 @@ def bd_lce_fwd(h, w, targets, lse=None, logp=None, workspace=None, stream=None):
     nbytes = bd_lce_workspace_bytes(N, V, Dm, 0)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
     s, sh = _stream(dev, stream)
-    st = lib().bd_lce_fwd(_ptr(h), _ptr(w), _ptr(targets), N, V, Dm, BD_ATTN_BF16, _ptr(l_), _ptr(lp), _ptr(ws),
+    kl = ctypes.c_void_p(None) if logits is None else _ptr(logits)
+    st = lib().bd_lce_fwd(_ptr(h), _ptr(w), _ptr(targets), N, V, Dm, BD_ATTN_BF16, _ptr(l_), _ptr(lp), kl, _ptr(ws),
                           ws.numel(), sh)
     if st:
         raise BdAttnError(st, "bd_lce_fwd")
@@ -398,9 +408,13 @@ def bd_lce_fwd(h, w, targets, lse=None, logp=None, workspace=None, stream=None):
     return l_, lp
 
 
-def bd_lce_bwd(h, w, targets, lse, dlogp, dh=None, dw=None, workspace=None, stream=None):
-    """dH [N, Dm] and dW [V, Dm] (bf16) for dLoss/dlogp = dlogp."""
+def bd_lce_bwd(h, w, targets, lse, dlogp, dh=None, dw=None, workspace=None, stream=None, logits=None):
+    """dH [N, Dm] and dW [V, Dm] (bf16) for dLoss/dlogp = dlogp (logits: the
+    buffer bd_lce_fwd filled, to skip recomputing them)."""
     N, V, Dm, dev = _lce_shapes(h, w, targets)
+    if logits is not None and (logits.dtype != torch.float32 or logits.numel() * 4 < bd_lce_logits_bytes(N, V, Dm)
+                               or not logits.is_contiguous() or logits.device != dev):
+        raise ValueError("logits: a contiguous float32 buffer of bd_lce_logits_bytes bytes on the device expected")
     _check("lse", lse, (N,), torch.float32, dev)
     _check("dlogp", dlogp, (N,), torch.float32, dev)
     dh_ = torch.empty_like(h) if dh is None else dh
@@ -410,7 +424,8 @@ def bd_lce_bwd(h, w, targets, lse, dlogp, dh=None, dw=None, workspace=None, stre
     nbytes = bd_lce_workspace_bytes(N, V, Dm, 1)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev) if workspace is None else workspace
     s, sh = _stream(dev, stream)
-    st = lib().bd_lce_bwd(_ptr(h), _ptr(w), _ptr(targets), _ptr(lse), _ptr(dlogp), N, V, Dm, BD_ATTN_BF16,
+    kl = ctypes.c_void_p(None) if logits is None else _ptr(logits)
+    st = lib().bd_lce_bwd(_ptr(h), _ptr(w), _ptr(targets), _ptr(lse), _ptr(dlogp), kl, N, V, Dm, BD_ATTN_BF16,
                           _ptr(dh_), _ptr(dw_), _ptr(ws), ws.numel(), sh)
     if st:
         raise BdAttnError(st, "bd_lce_bwd")
@@ -444,18 +459,25 @@ class LceFunction(torch.autograd.Function):
     """log p(target) through the LM head; differentiable in h and w."""
 
     @staticmethod
-    def forward(ctx, h, w, targets):
-        lse, logp = bd_lce_fwd(h, w, targets)
+    def forward(ctx, h, w, targets, keep_logits=False):
+        N, V, Dm, dev = _lce_shapes(h, w, targets)
+        logits = (torch.empty(bd_lce_logits_bytes(N, V, Dm) // 4, dtype=torch.float32, device=dev)
+                  if keep_logits else None)
+        lse, logp = bd_lce_fwd(h, w, targets, logits=logits)
         ctx.save_for_backward(h, w, targets, lse)
+        ctx.logits = logits
         return logp
 
     @staticmethod
     def backward(ctx, dlogp):
         h, w, targets, lse = ctx.saved_tensors
-        dh, dw = bd_lce_bwd(h, w, targets, lse, dlogp.contiguous().float())
-        return dh, dw, None
+        dh, dw = bd_lce_bwd(h, w, targets, lse, dlogp.contiguous().float(), logits=ctx.logits)
+        ctx.logits = None
+        return dh, dw, None, None
 
 
-def lm_head_logprobs(h, w, targets):
-    """Differentiable per-position log p(target) [N] float32 (targets outside [0, V): 0)."""
-    return LceFunction.apply(h, w, targets)
+def lm_head_logprobs(h, w, targets, keep_logits=False):
+    """Differentiable per-position log p(target) [N] float32 (targets outside
+    [0, V): 0).  keep_logits trades N x V float32 of memory for the
+    backward's recomputation of the logits."""
+    return LceFunction.apply(h, w, targets, keep_logits)

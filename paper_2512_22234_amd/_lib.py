@@ -52,9 +52,11 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_decode_workspace_bytes.restype = sz
     L.bd_attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci, ci]
     L.bd_lce_fwd.restype = ci
-    L.bd_lce_fwd.argtypes = [vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, sz, vp]
+    L.bd_lce_fwd.argtypes = [vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, vp, sz, vp]
     L.bd_lce_bwd.restype = ci
-    L.bd_lce_bwd.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, sz, vp]
+    L.bd_lce_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, vp, vp, vp, sz, vp]
+    L.bd_lce_logits_bytes.restype = sz
+    L.bd_lce_logits_bytes.argtypes = [ci, ci, ci, ci]
     L.bd_lce_workspace_bytes.restype = sz
     L.bd_lce_workspace_bytes.argtypes = [ci, ci, ci, ci, ci]
     L.bd_lce_objective.restype = ci

@@ -398,48 +398,60 @@ size_t bd_lce_workspace_bytes(int N, int V, int Dm, int dtype, int for_bwd) {
   return for_bwd ? bd::lce_bwd_workspace_bytes(s) : bd::lce_fwd_workspace_bytes(s);
 }
 
+size_t bd_lce_logits_bytes(int N, int V, int Dm, int dtype) {
+  bd::LceShape s;
+  if (validate_lce(N, V, Dm, dtype, s) != BD_ATTN_OK) return 0;
+  return bd::lce_logits_bytes(s);
+}
+
 int bd_lce_fwd(const void* H, const void* W, const int32_t* targets, int N, int V, int Dm, int dtype, float* lse,
-               float* logp, void* ws, size_t ws_bytes, hipStream_t stream) {
+               float* logp, float* logits, void* ws, size_t ws_bytes, hipStream_t stream) {
   bd::LceShape s;
   const int st = validate_lce(N, V, Dm, dtype, s);
   if (st != BD_ATTN_OK) return st;
   if (!H || !W || !targets || !lse || !logp || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(H, 16) || !aligned(W, 16) || !aligned(targets, 4) || !aligned(lse, 4) || !aligned(logp, 4) ||
-      !aligned(ws, 16))
+      !aligned(logits, 16) || !aligned(ws, 16))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   const size_t need = bd::lce_fwd_workspace_bytes(s);
   if (ws_bytes < need) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const Range in[] = {{H, (size_t)N * Dm * 2}, {W, (size_t)V * Dm * 2}, {targets, (size_t)N * 4}};
-  const Range out[] = {{lse, (size_t)N * 4}, {logp, (size_t)N * 4}, {ws, need}};
+  const Range out[] = {{lse, (size_t)N * 4}, {logp, (size_t)N * 4}, {ws, need},
+                       {logits, logits ? bd::lce_logits_bytes(s) : 0}};
   for (const Range& o : out)
     for (const Range& i : in)
-      if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
-  if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2])) return BD_ATTN_ERR_INVALID_ARGUMENT;
+      if (o.p && overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  for (int a = 0; a < 4; ++a)
+    for (int c = a + 1; c < 4; ++c)
+      if (out[a].p && out[c].p && overlap(out[a], out[c])) return BD_ATTN_ERR_INVALID_ARGUMENT;
   (void)hipGetLastError();
-  return bd::launch_lce_fwd(s, H, W, targets, lse, logp, ws, stream) == hipSuccess ? BD_ATTN_OK : BD_ATTN_ERR_HIP;
+  return bd::launch_lce_fwd(s, H, W, targets, lse, logp, logits, ws, stream) == hipSuccess ? BD_ATTN_OK
+                                                                                          : BD_ATTN_ERR_HIP;
 }
 
-int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* lse, const float* dlogp, int N,
-               int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes, hipStream_t stream) {
+int bd_lce_bwd(const void* H, const void* W, const int32_t* targets, const float* lse, const float* dlogp,
+               const float* logits, int N, int V, int Dm, int dtype, void* dH, void* dW, void* ws, size_t ws_bytes,
+               hipStream_t stream) {
   bd::LceShape s;
   const int st = validate_lce(N, V, Dm, dtype, s);
   if (st != BD_ATTN_OK) return st;
   if (!H || !W || !targets || !lse || !dlogp || !dH || !dW || !ws) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (!aligned(H, 16) || !aligned(W, 16) || !aligned(targets, 4) || !aligned(lse, 4) || !aligned(dlogp, 4) ||
-      !aligned(dH, 16) || !aligned(dW, 16) || !aligned(ws, 16))
+      !aligned(dH, 16) || !aligned(dW, 16) || !aligned(ws, 16) || !aligned(logits, 16))
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   const size_t need = bd::lce_bwd_workspace_bytes(s);
   if (ws_bytes < need) return BD_ATTN_ERR_WORKSPACE_TOO_SMALL;
   const Range in[] = {{H, (size_t)N * Dm * 2}, {W, (size_t)V * Dm * 2}, {targets, (size_t)N * 4},
-                      {lse, (size_t)N * 4}, {dlogp, (size_t)N * 4}};
+                      {lse, (size_t)N * 4}, {dlogp, (size_t)N * 4}, {logits, logits ? bd::lce_logits_bytes(s) : 0}};
   const Range out[] = {{dH, (size_t)N * Dm * 2}, {dW, (size_t)V * Dm * 2}, {ws, need}};
   for (const Range& o : out)
     for (const Range& i : in)
       if (overlap(o, i)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (overlap(out[0], out[1]) || overlap(out[0], out[2]) || overlap(out[1], out[2])) return BD_ATTN_ERR_INVALID_ARGUMENT;
   (void)hipGetLastError();
-  return bd::launch_lce_bwd(s, H, W, targets, lse, dlogp, dH, dW, ws, stream) == hipSuccess ? BD_ATTN_OK
-                                                                                          : BD_ATTN_ERR_HIP;
+  return bd::launch_lce_bwd(s, H, W, targets, lse, dlogp, logits, dH, dW, ws, stream) == hipSuccess
+             ? BD_ATTN_OK
+             : BD_ATTN_ERR_HIP;
 }
 
 int bd_lce_objective(const float* logp, const float* logp_old, const float* logp_ref, const float* adv,

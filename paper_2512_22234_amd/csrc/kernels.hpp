@@ -134,10 +134,12 @@ inline size_t lce_bwd_workspace_bytes(const LceShape& s) {
   return lce_align((size_t)s.N * lce_vocab_tiles(s) * 256 * 2);
 }
 
+// Kept logits (optional): float32 [N][V rounded up to 256].
+inline size_t lce_logits_bytes(const LceShape& s) { return (size_t)s.N * lce_vocab_tiles(s) * 256 * 4; }
 hipError_t launch_lce_fwd(const LceShape& s, const void* H, const void* W, const int* targets, float* lse,
-                          float* logp, void* ws, hipStream_t st);
+                          float* logp, float* logits, void* ws, hipStream_t st);
 hipError_t launch_lce_bwd(const LceShape& s, const void* H, const void* W, const int* targets, const float* lse,
-                          const float* coef, void* dH, void* dW, void* ws, hipStream_t st);
+                          const float* coef, const float* logits, void* dH, void* dW, void* ws, hipStream_t st);
 hipError_t launch_lce_objective(int N, int kind, float eps, float beta, const float* logp, const float* logp_old,
                                 const float* logp_ref, const float* adv, const float* weight, float* loss,
                                 float* dlogp, hipStream_t st);

@@ -27,6 +27,8 @@
 //   kernel  A side (MFMA A, output columns)  B side (MFMA B, output rows)  K    epilogue
 //   FWD     W, ROW (vocab)                   H, ROW (tokens)               Dm   (max, sum) per token and vocab tile
 //   REC     W, ROW                           H, ROW                        Dm   g -> G [N][Vp] bf16 (target entry afterwards)
+// (the forward can also keep its float32 logits, [N][Vp]; the backward then
+// forms g from them elementwise instead of running REC)
 //   DH      W, TR  (k = vocab, cols = d)     G, ROW (tokens)               Vp   dH [N][Dm]
 //   DW      H, TR  (k = tokens, cols = d)    G, TR  (k = tokens, vocab)    N    dW [V][Dm]
 #include "device.hpp"
@@ -56,6 +58,8 @@ struct LceParams {
   const float* coef;   // [N]
   const float* lse;    // [N]
   float* part;         // FWD: [N][nMT] (max in log2 units, sum)
+  float* logits;       // FWD: optional [N][ldl] float32 copy of the logits (null: not kept)
+  int ldl;
   bf16* C;             // REC: G [N][ldc]; STORE: dH or dW
   int ldc;
   int V;               // vocabulary size (FWD/REC: valid A-side columns)
@@ -254,6 +258,22 @@ __global__ __launch_bounds__(256, 1) void lce_gemm_kernel(LceParams p) {
   // other tiles take the unmasked path (a workgroup-uniform branch).
   const bool partial_cols = m0 + TB > p.V;
   if constexpr (EPI == EPI_FWD) {
+    if (p.logits != nullptr) {
+      // keep the logits for the backward pass (columns past V hold the zero rows' logits, 0)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n = n0 + 128 * wb + 32 * j + l32;
+        if (n < p.Nrows) {
+          float* lr = p.logits + (size_t)n * p.ldl + m0 + 128 * wa + 4 * g2;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4)
+              *reinterpret_cast<f32x4*>(lr + 32 * i + 8 * i4) =
+                  f32x4{acc[i][j][4 * i4], acc[i][j][4 * i4 + 1], acc[i][j][4 * i4 + 2], acc[i][j][4 * i4 + 3]};
+        }
+      }
+    }
     // per token: max and sum of exp over this tile's vocabulary columns (log2 units)
     auto stats = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
@@ -395,6 +415,30 @@ __global__ __launch_bounds__(256) void lce_merge_kernel(const float* part, const
   }
 }
 
+// g = -c exp(logit - LSE) from kept logits, bf16, zero past V (the target
+// entries are rewritten by lce_onehot_kernel).  One thread per 8 columns.
+__global__ __launch_bounds__(256) void lce_g_from_logits_kernel(const float* logits, const int* targets,
+                                                               const float* lse, const float* coef, int N, int V,
+                                                               int Vp, bf16* G) {
+  const size_t id = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int per = Vp / 8;
+  const size_t n = id / per;
+  if (n >= (size_t)N) return;
+  const int v0 = (int)(id % per) * 8;
+  const int t = targets[n];
+  const float ncf = (t >= 0 && t < V) ? -coef[n] : 0.f;
+  const float l2 = lse[n] * LOG2E;
+  const float* x = logits + n * Vp + v0;
+  const f32x4 a = *reinterpret_cast<const f32x4*>(x), b = *reinterpret_cast<const f32x4*>(x + 4);
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float xe = e < 4 ? a[e] : b[e - 4];
+    o[e] = (bf16)(v0 + e < V ? ncf * fast_exp2(xe * LOG2E - l2) : 0.f);
+  }
+  *reinterpret_cast<bf16x8*>(G + n * Vp + v0) = o;
+}
+
 // The target entry of g: c (1 - p_t), from the target logit in float32 (the
 // tile epilogue wrote -c p_t there).  One wave per token.
 __global__ __launch_bounds__(256) void lce_onehot_kernel(const bf16* H, const bf16* W, const int* targets,
@@ -458,7 +502,7 @@ hipError_t launch_gemm(const LceParams& p, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_lce_fwd(const LceShape& s, const void* H, const void* W, const int* targets, float* lse,
-                          float* logp, void* ws, hipStream_t st) {
+                          float* logp, float* logits, void* ws, hipStream_t st) {
   LceParams p{};
   p.A = static_cast<const bf16*>(W);
   p.B = static_cast<const bf16*>(H);
@@ -473,6 +517,8 @@ hipError_t launch_lce_fwd(const LceShape& s, const void* H, const void* W, const
   p.targets = targets;
   char* w = static_cast<char*>(ws);
   p.part = reinterpret_cast<float*>(w + lce_fwd_part_offset(s));
+  p.logits = logits;
+  p.ldl = lce_vocab_tiles(s) * TB;
   p.V = s.V;
   hipError_t e = launch_gemm<EPI_FWD, false, false>(p, st);
   if (e != hipSuccess) return e;
@@ -490,7 +536,7 @@ hipError_t launch_lce_objective(int N, int kind, float eps, float beta, const fl
 }
 
 hipError_t launch_lce_bwd(const LceShape& s, const void* H, const void* W, const int* targets, const float* lse,
-                          const float* coef, void* dH, void* dW, void* ws, hipStream_t st) {
+                          const float* coef, const float* logits, void* dH, void* dW, void* ws, hipStream_t st) {
   const int Vp = lce_vocab_tiles(s) * TB;
   bf16* G = reinterpret_cast<bf16*>(static_cast<char*>(ws) + lce_bwd_g_offset(s));
   // G = coef (onehot - softmax), [N][Vp] (columns past V zero)
@@ -511,7 +557,15 @@ hipError_t launch_lce_bwd(const LceShape& s, const void* H, const void* W, const
   p.C = G;
   p.ldc = Vp;
   p.V = s.V;
-  hipError_t e = launch_gemm<EPI_REC, false, false>(p, st);
+  hipError_t e;
+  if (logits != nullptr) {
+    const size_t threads = (size_t)s.N * (Vp / 8);
+    hipLaunchKernelGGL(lce_g_from_logits_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, logits,
+                       targets, lse, coef, s.N, s.V, Vp, G);
+    e = hipGetLastError();
+  } else {
+    e = launch_gemm<EPI_REC, false, false>(p, st);
+  }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lce_onehot_kernel, dim3(cdiv(s.N, 4)), dim3(256), 0, st, p.B, p.A, targets, lse, coef, s.N,
                      s.V, s.Dm, G, Vp);

@@ -231,7 +231,8 @@ def _lce_fwd(**kw):
     a.update(kw)
     vp = ctypes.c_void_p
     return _lib.lib().bd_lce_fwd(vp(a["H"]), vp(a["W"]), vp(a["t"]), a["N"], a["V"], a["Dm"], a["dtype"],
-                                 vp(a["lse"]), vp(a["logp"]), vp(a["ws"]), a["ws_bytes"], vp(a["stream"]))
+                                 vp(a["lse"]), vp(a["logp"]), vp(a.get("logits", 0)), vp(a["ws"]), a["ws_bytes"],
+                                 vp(a["stream"]))
 
 
 def _lce_bwd(**kw):
@@ -239,7 +240,8 @@ def _lce_bwd(**kw):
              dH=A + 5 * SZ, dW=A + 6 * SZ, ws=A + 7 * SZ, ws_bytes=1 << 30, stream=None)
     a.update(kw)
     vp = ctypes.c_void_p
-    return _lib.lib().bd_lce_bwd(vp(a["H"]), vp(a["W"]), vp(a["t"]), vp(a["lse"]), vp(a["dl"]), a["N"], a["V"],
+    return _lib.lib().bd_lce_bwd(vp(a["H"]), vp(a["W"]), vp(a["t"]), vp(a["lse"]), vp(a["dl"]), vp(a.get("logits", 0)),
+                                 a["N"], a["V"],
                                  a["Dm"], a["dtype"], vp(a["dH"]), vp(a["dW"]), vp(a["ws"]), a["ws_bytes"],
                                  vp(a["stream"]))
 
@@ -250,6 +252,9 @@ def _lce_bwd(**kw):
     (dict(logp=A + 16), 1),                # output overlaps H
     (dict(ws=A + 3 * SZ + 16), 1),         # workspace overlaps LSE
     (dict(ws_bytes=64), 3),
+    (dict(logits=A + 8 * SZ + 4), 1),      # misaligned kept logits
+    (dict(logits=A + 16), 1),              # kept logits overlap H
+    (dict(logits=A + 5 * SZ), 1),          # kept logits overlap the workspace
 ])
 def test_lce_fwd_validation(kw, status):
     assert _lce_fwd(**kw) == status
@@ -260,6 +265,7 @@ def test_lce_fwd_validation(kw, status):
     (dict(dW=A + SZ + 64), 1),             # dW overlaps W
     (dict(dH=A + 6 * SZ), 1),              # dH overlaps dW
     (dict(ws_bytes=1000), 3),
+    (dict(logits=A + 8 * SZ, dW=A + 8 * SZ + 256), 1),   # dW overlaps the kept logits
 ])
 def test_lce_bwd_validation(kw, status):
     assert _lce_bwd(**kw) == status

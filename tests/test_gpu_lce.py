@@ -67,6 +67,32 @@ def test_lce_matches_oracle(N, V, Dm):
     assert np.all(_np(logp)[unscored] == 0) and np.all(_np(dh)[unscored] == 0)
 
 
+@pytest.mark.parametrize("N,V,Dm", [(100, 1000, 256), (513, 2048, 768)])
+def test_lce_kept_logits_match_recompute(N, V, Dm):
+    """The backward from kept logits agrees with the recomputing one and with
+    the oracle; the kept logits themselves are the oracle's logits."""
+    from paper_2512_22234_amd import bd_lce_logits_bytes
+    h, w, t = make_lce_inputs(N, V, Dm, seed=500 + N)
+    t[::5] = -1
+    c = torch.randn(N, generator=torch.Generator().manual_seed(7), dtype=torch.float32)
+    hd, wd, td, cd = h.to(DEV), w.to(DEV), t.to(DEV), c.to(DEV)
+    keep = torch.empty(bd_lce_logits_bytes(N, V, Dm) // 4, dtype=torch.float32, device=DEV)
+    lse, logp = bd_lce_fwd(hd, wd, td, logits=keep)
+    lse2, logp2 = bd_lce_fwd(hd, wd, td)
+    dh_k, dw_k = bd_lce_bwd(hd, wd, td, lse, cd, logits=keep)
+    dh_r, dw_r = bd_lce_bwd(hd, wd, td, lse, cd)
+    torch.cuda.synchronize()
+    assert torch.equal(lse, lse2) and torch.equal(logp, logp2)  # keeping the logits changes nothing else
+    H, W = h.double().numpy(), w.double().numpy()
+    Vp = keep.numel() // N
+    kept = keep.view(N, Vp)[:, :V].double().cpu().numpy()
+    assert np.abs(kept - H @ W.T).max() <= 1e-4 * max(1.0, np.abs(H @ W.T).max())
+    dH_o, dW_o = oracle.lm_head_backward(H, W, t.numpy(), c.double().numpy())
+    for got, want in ((dh_k, dH_o), (dw_k, dW_o), (dh_r, dH_o), (dw_r, dW_o)):
+        assert _rel(_np(got), want) <= G_REL
+    assert _rel(_np(dh_k), _np(dh_r)) <= 2e-3 and _rel(_np(dw_k), _np(dw_r)) <= 2e-3
+
+
 def test_lce_deterministic():
     h, w, t = (x.to(DEV) for x in make_lce_inputs(700, 3000, 512, seed=41))
     c = torch.randn(700, device=DEV)
@@ -161,7 +187,7 @@ def test_lce_invalid_arguments():
     ws = torch.empty(need, dtype=torch.uint8, device=DEV)
     st = lib().bd_lce_fwd(ctypes.c_void_p(h.data_ptr()), ctypes.c_void_p(w.data_ptr()), ctypes.c_void_p(t.data_ptr()),
                           8, 300, 256, BD_ATTN_FP32, ctypes.c_void_p(lse.data_ptr()),
-                          ctypes.c_void_p(logp.data_ptr()), ctypes.c_void_p(ws.data_ptr()), need, None)
+                          ctypes.c_void_p(logp.data_ptr()), None, ctypes.c_void_p(ws.data_ptr()), need, None)
     assert st == 2
     with pytest.raises(BdAttnError) as e:
         bd_lce_objective(lse, lse, BD_LCE_DIPO)  # DiPO needs logp_old and adv
