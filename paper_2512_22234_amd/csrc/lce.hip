@@ -43,7 +43,9 @@ constexpr int NST = 4;                // LDS ring stages
 constexpr uint32_t OPB = TB * BK * 2;  // bytes of one operand tile (16 KB)
 constexpr int RED_STRIDE = TB + 8;    // staging row stride (bf16) of the output tile: 528 bytes
 
-enum Epi { EPI_FWD = 0, EPI_REC = 1, EPI_STORE = 2 };
+// EPI_FWD_KEEP is EPI_FWD that also stores the float32 logits (a variant of
+// its own, so the plain forward's epilogue carries none of its registers)
+enum Epi { EPI_FWD = 0, EPI_REC = 1, EPI_STORE = 2, EPI_FWD_KEEP = 3 };
 
 struct LceParams {
   const bf16* A;  // A-side source
@@ -254,12 +256,40 @@ __global__ __launch_bounds__(256, 1) void lce_gemm_kernel(LceParams p) {
 
   // acc[i][j][4 i4 + jj]: A-side column  m0 + 128 wa + 32 i + 8 i4 + 4 g2 + jj,
   //                       B-side row     n0 + 128 wb + 32 j + l32
-  // Columns past the vocabulary exist only in the last vocabulary tile; the
-  // other tiles take the unmasked path (a workgroup-uniform branch).
+  // Columns past the vocabulary exist only in the last vocabulary tile.
   const bool partial_cols = m0 + TB > p.V;
-  if constexpr (EPI == EPI_FWD) {
-    if (p.logits != nullptr) {
-      // keep the logits for the backward pass (columns past V hold the zero rows' logits, 0)
+  if constexpr (EPI == EPI_FWD || EPI == EPI_FWD_KEEP) {
+    // per token: max and sum of exp over this tile's vocabulary columns (log2
+    // units).  Every tile takes the masked path: a branch between a masked and
+    // an unmasked copy makes the compiler move all 256 accumulators into VGPRs
+    // ahead of it, which spills.
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // scores recomputed from the accumulators in each pass (nothing is
+      // written back, so no block's values stay live longer)
+      auto score = [&](int i, int e) __attribute__((always_inline)) {
+        const int v = m0 + 128 * wa + 32 * i + 8 * (e >> 2) + 4 * g2 + (e & 3);
+        return v < p.V ? acc[i][j][e] * LOG2E : -INFINITY;
+      };
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, score(i, e));
+      mx = halves_max(mx);
+      float sum = 0.f;
+      if (mx != -INFINITY) {  // (a wave half past the last vocabulary row has no columns)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sum += fast_exp2(score(i, e) - mx);  // exp2(-inf) = 0
+      }
+      sum = halves_sum(sum);
+      if (g2 == 0) sm.red[wa][128 * wb + 32 * j + l32] = float2{mx, sum};
+    }
+    if constexpr (EPI == EPI_FWD_KEEP) {
+      // the logits for the backward pass (columns past V hold the zero rows'
+      // logits, 0)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int n = n0 + 128 * wb + 32 * j + l32;
@@ -274,38 +304,7 @@ __global__ __launch_bounds__(256, 1) void lce_gemm_kernel(LceParams p) {
         }
       }
     }
-    // per token: max and sum of exp over this tile's vocabulary columns (log2 units)
-    auto stats = [&](auto masked) __attribute__((always_inline)) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            float x = acc[i][j][e] * LOG2E;
-            if constexpr (decltype(masked)::value) {
-              const int v = m0 + 128 * wa + 32 * i + 8 * (e >> 2) + 4 * g2 + (e & 3);
-              x = v < p.V ? x : -INFINITY;
-            }
-            acc[i][j][e] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = halves_max(mx);
-        float sum = 0.f;
-        if (mx != -INFINITY) {  // (a wave half past the last vocabulary row has no columns)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) sum += fast_exp2(acc[i][j][e] - mx);  // exp2(-inf) = 0
-        }
-        sum = halves_sum(sum);
-        if (g2 == 0) sm.red[wa][128 * wb + 32 * j + l32] = float2{mx, sum};
-      }
-    };
-    if (partial_cols) stats(Flag<true>());
-    else stats(Flag<false>());
-    __syncthreads();
+    barrier_lds_only();  // (the kept-logits stores need not have landed: only LDS is exchanged)
     // two halves of the vocabulary tile -> one partial per token
     const int n = n0 + tid;
     if (n < p.Nrows) {
@@ -351,7 +350,7 @@ __global__ __launch_bounds__(256, 1) void lce_gemm_kernel(LceParams p) {
     };
     if (EPI == EPI_REC && partial_cols) stage(Flag<true>());
     else stage(Flag<false>());
-    __syncthreads();
+    barrier_lds_only();  // the staged tile is in LDS
     // write rows of 256 columns (512 bytes): 16 lanes a row, 16 bytes each
     const int cr = (tid & 15) * 16;
 #pragma unroll 4
@@ -520,7 +519,8 @@ hipError_t launch_lce_fwd(const LceShape& s, const void* H, const void* W, const
   p.logits = logits;
   p.ldl = lce_vocab_tiles(s) * TB;
   p.V = s.V;
-  hipError_t e = launch_gemm<EPI_FWD, false, false>(p, st);
+  hipError_t e = logits != nullptr ? launch_gemm<EPI_FWD_KEEP, false, false>(p, st)
+                                    : launch_gemm<EPI_FWD, false, false>(p, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lce_merge_kernel, dim3(cdiv(s.N, 4)), dim3(256), 0, st, p.part, p.B, p.A, targets, s.N, p.nMT,
                      s.V, s.Dm, lse, logp);
