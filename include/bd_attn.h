@@ -130,6 +130,18 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
 int bd_attn_mask_windows_host(int L, int S, int by_key, int8_t* out);
 
 /*
+ * Tests only: the visibility windows of runs of `group` consecutive positions
+ * of one half (the runs start at multiples of `group`; the last one of a half
+ * may be shorter), i.e. the union over the run's rows of the windows above,
+ * expanded into the same 2L x 2L layout: out[q * 2L + k] = 1 iff key k is
+ * visible from some query of q's run (by_key = 0), or some key of k's run is
+ * visible from query q (by_key = 1).  The kernels skip, per wave, the 32-key
+ * or 32-query blocks outside the window of the wave's own 32-row run.
+ * Returns BD_ATTN_ERR_INVALID_ARGUMENT for L, S or group < 1 or a null `out`.
+ */
+int bd_attn_group_windows_host(int L, int S, int by_key, int group, int8_t* out);
+
+/*
  * Benchmark variants of bd_attn_fwd / bd_attn_bwd: identical work and
  * validation, and in addition hipEventRecord(marks[i], stream) for caller-
  * created events: marks[0] before the first kernel launch and marks[i] right

@@ -105,6 +105,14 @@ def bd_attn_mask_windows_host(L: int, S: int, by_key: bool) -> np.ndarray:
     return out
 
 
+def bd_attn_group_windows_host(L: int, S: int, by_key: bool, group: int) -> np.ndarray:
+    out = np.zeros((2 * L, 2 * L), dtype=np.int8)
+    st = lib().bd_attn_group_windows_host(L, S, int(by_key), group, out.ctypes.data_as(ctypes.c_void_p))
+    if st:
+        raise BdAttnError(st, "bd_attn_group_windows_host")
+    return out
+
+
 def _shapes(q, k, L):
     if q.dim() != 4 or k.dim() != 4:
         raise ValueError("q [B,Hq,2L,D] and k/v [B,Hkv,2L,D] expected")

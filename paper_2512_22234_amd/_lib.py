@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_visit_lists_host.argtypes = [ci, ci, ci, ci, ci, vp]
     L.bd_attn_mask_windows_host.restype = ci
     L.bd_attn_mask_windows_host.argtypes = [ci, ci, ci, vp]
+    L.bd_attn_group_windows_host.restype = ci
+    L.bd_attn_group_windows_host.argtypes = [ci, ci, ci, ci, vp]
     L.bd_attn_status_string.restype = ctypes.c_char_p
     L.bd_attn_status_string.argtypes = [ci]
     L.bd_attn_version.restype = ci

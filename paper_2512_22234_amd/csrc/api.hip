@@ -301,6 +301,26 @@ int bd_attn_mask_windows_host(int L, int S, int by_key, int8_t* out) {
   return BD_ATTN_OK;
 }
 
+int bd_attn_group_windows_host(int L, int S, int by_key, int group, int8_t* out) {
+  if (L < 1 || S < 1 || group < 1 || out == nullptr) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (S > L) S = L;
+  const int N = 2 * L;
+  memset(out, 0, (size_t)N * N);
+  for (int a = 0; a < N; ++a) {  // the row's own position; its run is [r0, r1) of its half
+    const int ah = a / L, ap = a % L, r0 = (ap / group) * group, r1 = bd::imin(L, r0 + group);
+    for (int oh = 0; oh < 2; ++oh) {
+      const bd::PosWindow win = by_key ? bd::wave_queries_seeing(ah, oh, r0, r1, L, S)
+                                       : bd::wave_keys_visible(ah, oh, r0, r1, L, S);
+      for (int x = win.lo; x < win.hi; ++x) {
+        const int other = oh * L + x;
+        if (by_key) out[(size_t)other * N + a] = 1;
+        else out[(size_t)a * N + other] = 1;
+      }
+    }
+  }
+  return BD_ATTN_OK;
+}
+
 int bd_attn_fwd(const void* Q, const void* K, const void* V, int B, int L, int S, int Hq, int Hkv, int D,
                 float scale, int dtype, void* O, float* LSE, void* ws, size_t ws_bytes, hipStream_t stream) {
   bd::Shape s;

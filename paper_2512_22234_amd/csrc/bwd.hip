@@ -467,7 +467,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   const size_t qrow = qrow0 + hq * hrows + prow;
 
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
-  const int T = kl.count();
+  const int T = __builtin_amdgcn_readfirstlane(kl.count());  // (uniform; keeps the step loops scalar)
   const TileCopy<D, BN, 256> copy(tid);
   const bf16* const kbase = p.K + kvbase;
   const bf16* const vbase = p.V + kvbase;
@@ -478,7 +478,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
     return kh * L + j * BN;
   };
   auto issue = [&](int t, char* kdst, char* vdst) {
-    const int r = tile_row(t);
+    const int r = __builtin_amdgcn_readfirstlane(tile_row(t));  // (scalar buffer descriptors)
     copy.issue_rows(kbase + (size_t)r * D, N - r, kdst);
     copy.issue_rows(vbase + (size_t)r * D, N - r, vdst);
   };
@@ -513,21 +513,22 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
   wait_global_loads();
   __syncthreads();
 
-  // Per-step bookkeeping as in the forward kernel: a two-comparison FULL
-  // test (the visibility window is only needed, and computed, on PARTIAL
-  // tiles: this kernel has no registers to spare for caching it).
+  // The walk as in the forward kernel: first the key tiles FULL for the
+  // whole query tile, in a loop with no visibility test, then the diagonal
+  // ones, one 32-key block at a time, each wave skipping the blocks none of
+  // its rows sees (wave-uniform windows; the per-row window is computed in
+  // those steps only: this kernel has no registers to spare for caching it).
   const FullRange fr = full_range_vs_query_tile(qh, q0, q1, L, S, BM);
+  const int wr0 = q0 + 32 * __builtin_amdgcn_readfirstlane(w), wr1 = imin(q1, wr0 + 32);
+  const PosWindow uw_n = wave_keys_visible(qh, HALF_NOISY, wr0, wr1, L, S);
+  const PosWindow uw_c = wave_keys_visible(qh, HALF_CLEAN, wr0, wr1, L, S);
 
-  // One key tile; restrict-qualified current and next buffers as in the
+  // One FULL key tile; restrict-qualified current and next buffers as in the
   // forward kernel, so the copy in flight does not make the compiler wait
   // before the reads of the current tile.  The copy of the next tile is
   // spread between the MFMAs (the last step copies its own tile again).
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
                        char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
-    int kh, j;
-    kl.at(t, kh, j);
-    const int k0 = j * BN;
-    const bool full = fr.full(kh, k0, BN);
     {
       f32x16 sacc[KB], dpacc[KB];
 #pragma unroll
@@ -538,7 +539,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
           dpacc[kb][e] = 0.f;
         }
       // the next tile's copy, one instruction per step of the loop below
-      const int rn = tile_row(imin(t + 1, T - 1));
+      const int rn = __builtin_amdgcn_readfirstlane(tile_row(imin(t + 1, T - 1)));
       const __amdgpu_buffer_rsrc_t kn = make_buffer(kbase + (size_t)rn * D, (uint32_t)((N - rn) * D * 2));
       const __amdgpu_buffer_rsrc_t vn = make_buffer(vbase + (size_t)rn * D, (uint32_t)((N - rn) * D * 2));
       // S^T[key][q] = sum_d K[key][d] Q[q][d];  dP^T[key][q] = sum_d V[key][d] dO[q][d]
@@ -560,26 +561,11 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       // operand reads four MFMAs ahead (a read's latency exceeds one MFMA),
       // the copy spread between the MFMAs
       pipeline_reads_and_copies<2 * DS * KB, 4, 1, DQ_COPIES>();
-      // dS = P (dP - delta); FULL tiles without the per-element visibility test
-      const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
-      const unsigned span = (unsigned)(win.hi - win.lo);
-      const int rel = k0 + 4 * g2 - win.lo;
-      auto ds = [&](auto masked) __attribute__((always_inline)) {
+      // dS = P (dP - delta), every pair visible
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-              const int e = 4 * i + jj;
-              float pv = fast_exp2(sacc[kb][e] * p.c - lse2);
-              if constexpr (decltype(masked)::value) pv = (unsigned)(rel + kb * 32 + 8 * i + jj) < span ? pv : 0.f;
-              sacc[kb][e] = pv * (dpacc[kb][e] - dlt);
-            }
-      };
-      // (EMPTY is never visited; it would take the masked path, which masks all of it)
-      if (full) ds(Flag<false>());
-      else ds(Flag<true>());
+        for (int e = 0; e < 16; ++e) sacc[kb][e] = fast_exp2(sacc[kb][e] * p.c - lse2) * (dpacc[kb][e] - dlt);
       bf16x8 dsb[PC];
 #pragma unroll
       for (int c = 0; c < PC; ++c) dsb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
@@ -590,13 +576,66 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
         for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(kcur, ops.tr_rel0, ops.tr_rel1, c, db), dsb[c], dqacc[db]);
     }
   };
-  for (int t = 0; t < T; ++t) {
-    char* cur = lds + (t & 1) * TILE;
-    char* nxt = lds + ((t + 1) & 1) * TILE;
-    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
+  // One 32-key block kb of a diagonal key tile (the next tile's copy is
+  // issued by the caller).
+  auto block_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, int kh, int k0, int kb)
+                        __attribute__((always_inline)) {
+    f32x16 sa, dpa;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      sa[e] = 0.f;
+      dpa[e] = 0.f;
+    }
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      sa = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sa);
+      dpa = mfma32(lds_rows<D>(vcur, ops.row_rel, s, kb), doreg[s], dpa);
+    }
+    pipeline_lds_reads<2 * DS, 4, 1>();
+    // dS = P (dP - delta) on the visible pairs, 0 elsewhere
+    const PosWindow win = keys_visible_from(qh, kh, qblock0, L, S, qvalid);
+    const unsigned span = (unsigned)(win.hi - win.lo);
+    const int rel = k0 + 32 * kb + 4 * g2 - win.lo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int e = 4 * i + jj;
+        float pv = fast_exp2(sa[e] * p.c - lse2);
+        pv = (unsigned)(rel + 8 * i + jj) < span ? pv : 0.f;
+        sa[e] = pv * (dpa[e] - dlt);
+      }
+    const bf16x8 d0 = pack8(sa, 0), d1 = pack8(sa, 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(kcur, ops.tr_rel0, ops.tr_rel1, 2 * kb, db), d0, dqacc[db]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      dqacc[db] = mfma32(lds_tr<D>(kcur, ops.tr_rel0, ops.tr_rel1, 2 * kb + 1, db), d1, dqacc[db]);
+  };
+  auto end_step = [&]() __attribute__((always_inline)) {
     compute_fence();
     wait_global_loads();
     __syncthreads();
+  };
+  const int t_main = __builtin_amdgcn_readfirstlane(imin(T, fr.full_prefix(BN)));
+  for (int t = 0; t < t_main; ++t) {
+    char* cur = lds + (t & 1) * TILE;
+    char* nxt = lds + ((t + 1) & 1) * TILE;
+    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
+    end_step();
+  }
+  for (int t = t_main; t < T; ++t) {
+    char* cur = lds + (t & 1) * TILE;
+    char* nxt = lds + ((t + 1) & 1) * TILE;
+    int kh, j;
+    kl.at(t, kh, j);
+    const int k0 = j * BN;
+    const PosWindow uw = kh == HALF_NOISY ? uw_n : uw_c;
+    issue(imin(t + 1, T - 1), nxt, nxt + 2 * TILE);
+#pragma unroll 1
+    for (int kb = 0; kb < KB; ++kb)  // (not unrolled: one block body in the loop)
+      if (k0 + 32 * kb < uw.hi && k0 + 32 * kb + 32 > uw.lo) block_step(cur, cur + 2 * TILE, kh, k0, kb);
+    end_step();
   }
 
   if (qvalid) {

@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const int prow = qh * L + r;
 
   const KeyTileList kl = key_tiles_for_query_tile(qh, qi, L, S, BM, BN);
-  const int T = kl.count();
+  const int T = __builtin_amdgcn_readfirstlane(kl.count());  // (uniform; keeps the step loops scalar)
   const TileCopy<D, BN, 256> copy(tid);
   const bf16* const kbase = p.K + kvbase;
   const bf16* const vbase = p.V + kvbase;
@@ -99,7 +99,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   };
   // copy key tile t of K or V
   auto issue = [&](int t, bool is_v, char* dst) {
-    const int r = tile_row(t);
+    // (the row is the same for every lane; saying so keeps the copy's buffer
+    // descriptor scalar where the compiler cannot prove it)
+    const int r = __builtin_amdgcn_readfirstlane(tile_row(t));
     copy.issue_rows((is_v ? vbase : kbase) + (size_t)r * D, N - r, dst);
   };
 
@@ -133,6 +135,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const FullRange fr = full_range_vs_query_tile(qh, q0, q1, L, S, BM);
   const PosWindow win_n = keys_visible_from(qh, HALF_NOISY, qblock0, L, S, qvalid);
   const PosWindow win_c = keys_visible_from(qh, HALF_CLEAN, qblock0, L, S, qvalid);
+  // The keys any row of this wave can see, per half (a wave-uniform union of
+  // the rows' windows): on the diagonal tiles a 32-key block outside it is
+  // skipped by this wave, MFMAs and softmax alike (its probabilities would all
+  // be 0).  This leaves 10 of 16 wave-blocks of work in the clean quadrants'
+  // diagonal tiles and 4 of 16 in the noisy-noisy ones (at S dividing 32).
+  const int wr0 = q0 + 32 * __builtin_amdgcn_readfirstlane(w), wr1 = imin(q1, wr0 + 32);
+  const PosWindow uw_n = wave_keys_visible(qh, HALF_NOISY, wr0, wr1, L, S);
+  const PosWindow uw_c = wave_keys_visible(qh, HALF_CLEAN, wr0, wr1, L, S);
 
   // One key tile.  The current K/V tiles and the buffers the next tile is
   // copied into are distinct restrict-qualified pointers: the alias scopes
@@ -147,14 +157,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   // The last step copies its own tile again (into the buffer nothing reads
   // afterwards), which keeps the step straight-line code.
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
-                       char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
+                       char* __restrict__ vnxt, int t, bool full, int kh, int k0) __attribute__((always_inline)) {
     const int tn = imin(t + 1, T - 1);
-    int kh, j;
-    kl.at(t, kh, j);
-    const int k0 = j * BN;
-    // (EMPTY tiles are never visited; were one visited, the window test of
-    // PARTIAL tiles would mask all of it)
-    const bool full = fr.full(kh, k0, BN);
     {
       f32x16 sacc[KB];
 #pragma unroll
@@ -226,13 +230,97 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       interleave_copies<PC * DB, decltype(copy)::NI>();
     }
   };
-  for (int t = 0; t < T; ++t) {
-    char* cur = lds + (t & 1) * TILE;
-    char* nxt = lds + ((t + 1) & 1) * TILE;
-    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
+  // One 32-key block kb of a key tile, for the diagonal tiles: the same
+  // arithmetic as a tile step restricted to those keys (masked by the window).
+  // The next tile's copy is issued by the caller.
+  auto block_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, int kh, int k0, int kb)
+                        __attribute__((always_inline)) {
+    f32x16 sa;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sa[e] = 0.f;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) sa = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sa);
+    pipeline_lds_reads<DS, 4, 1>();
+    const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
+    const unsigned span = (unsigned)(win.hi - win.lo);
+    const int rel = k0 + 32 * kb + 4 * g2 - win.lo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const unsigned pos = (unsigned)(rel + 8 * i + jj);
+        sa[4 * i + jj] = pos < span ? sa[4 * i + jj] : -INFINITY;
+      }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sa[e], sa[e + 1]));
+    mx = halves_max(mx) * p.c;
+    const bool grow = mx > m + RESCALE_SLACK;
+    if (__any(grow)) {
+      asm volatile("" ::: "memory");
+      const float alpha = grow ? fast_exp2(m - mx) : 1.f;
+      const float mnew = grow ? mx : m;
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
+      m = mnew;
+    }
+    const float muse = (m == -INFINITY) ? 0.f : m;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float x = fast_exp2(sa[e] * p.c - muse);
+      sa[e] = x;
+      lsum += x;
+    }
+    const bf16x8 p0 = pack8(sa, 0), p1 = pack8(sa, 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, 2 * kb, db), p0, oacc[db]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, 2 * kb + 1, db), p1, oacc[db]);
+  };
+  auto step_buffers = [&](int t, char*& cur, char*& nxt) __attribute__((always_inline)) {
+    cur = lds + (t & 1) * TILE;
+    nxt = lds + ((t + 1) & 1) * TILE;
+  };
+  auto end_step = [&]() __attribute__((always_inline)) {
     compute_fence();
     wait_global_loads();  // this wave's part of the next tile has landed in LDS
     __syncthreads();      // ... for every wave, and every wave is done with this buffer
+  };
+  // The walk starts with the key tiles that are FULL for the whole query tile
+  // (clean keys of earlier blocks); one loop with a single step body runs
+  // them.  The remaining few tiles (the diagonal ones) run in a second loop
+  // whose steps skip, per wave, the 32-key blocks none of its rows sees.
+  // Keeping the two apart keeps the register assignment of the main loop
+  // free of the copies that merging several step bodies in one loop costs.
+  const int t_main = __builtin_amdgcn_readfirstlane(imin(T, fr.full_prefix(BN)));
+  for (int t = 0; t < t_main; ++t) {
+    char *cur, *nxt;
+    step_buffers(t, cur, nxt);
+    int kh, j;
+    kl.at(t, kh, j);
+    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t, true, kh, j * BN);
+    end_step();
+  }
+  for (int t = t_main; t < T; ++t) {
+    char *cur, *nxt;
+    step_buffers(t, cur, nxt);
+    int kh, j;
+    kl.at(t, kh, j);
+    const int k0 = j * BN;
+    // (EMPTY tiles are never visited; were one visited, the window test of
+    // PARTIAL tiles would mask all of it)
+    const PosWindow uw = kh == HALF_NOISY ? uw_n : uw_c;
+    const int tn = imin(t + 1, T - 1);
+    issue(tn, false, nxt);
+    issue(tn, true, nxt + 2 * TILE);
+#pragma unroll 1
+    for (int kb = 0; kb < KB; ++kb)  // (not unrolled: one block body in the loop)
+      if (k0 + 32 * kb < uw.hi && k0 + 32 * kb + 32 > uw.lo) block_step(cur, cur + 2 * TILE, kh, k0, kb);
+    end_step();
   }
 
   const float lt = halves_sum(lsum);

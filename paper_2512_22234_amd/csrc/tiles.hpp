@@ -116,6 +116,9 @@ struct FullRange {
   BD_HD bool full(int half, int x0, int n) const {
     return half == HALF_NOISY ? (x0 >= lo_n && x0 + n <= hi_n) : (x0 >= lo_c && x0 + n <= hi_c);
   }
+  // With the fixed tile a query tile: the number of leading clean key tiles
+  // of size n (the walk's first tiles) that are FULL.
+  BD_HD int full_prefix(int n) const { return lo_c == 0 && hi_c > 0 ? hi_c / n : 0; }
 };
 // Fixed key tile [k0, k1) of half kh (full-sized iff k1 - k0 == BN); moving query tiles.
 BD_HD FullRange full_range_vs_key_tile(int kh, int k0, int k1, int L, int S, int BN) {
@@ -171,6 +174,27 @@ BD_HD PosWindow queries_seeing(int kh, int qh, int a, int L, int S, bool valid) 
   if (!valid) return {0, 0};
   if (qh == HALF_NOISY) return kh == HALF_NOISY ? PosWindow{a, imin(L, a + S)} : PosWindow{imin(L, a + S), L};
   return kh == HALF_CLEAN ? PosWindow{a, L} : PosWindow{0, 0};
+}
+
+// Unions of those windows over a run of consecutive positions [r0, r1) of one
+// half (empty when r0 >= r1).  Each row's window is an interval and the
+// windows of consecutive rows are either nested or adjacent, so the union is
+// again one interval, and it is exactly the set of positions that some row of
+// the run sees (or is seen by).
+// Keys of half kh visible from some query of [r0, r1) in half qh.
+BD_HD PosWindow wave_keys_visible(int qh, int kh, int r0, int r1, int L, int S) {
+  if (r0 >= r1) return {0, 0};
+  const int a0 = (r0 / S) * S, a1 = ((r1 - 1) / S) * S;  // block starts of the first and last row
+  if (qh == HALF_NOISY) return kh == HALF_NOISY ? PosWindow{a0, imin(L, a1 + S)} : PosWindow{0, a1};
+  return kh == HALF_CLEAN ? PosWindow{0, imin(L, a1 + S)} : PosWindow{0, 0};
+}
+// Queries of half qh that see some key of [r0, r1) in half kh.
+BD_HD PosWindow wave_queries_seeing(int kh, int qh, int r0, int r1, int L, int S) {
+  if (r0 >= r1) return {0, 0};
+  const int a0 = (r0 / S) * S, a1 = ((r1 - 1) / S) * S;
+  if (qh == HALF_NOISY)
+    return kh == HALF_NOISY ? PosWindow{a0, imin(L, a1 + S)} : PosWindow{imin(L, a0 + S), L};
+  return kh == HALF_CLEAN ? PosWindow{a0, L} : PosWindow{0, 0};
 }
 
 // Key tiles visited by query tile (qh, i): clean key tiles [0, nclean) then,

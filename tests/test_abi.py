@@ -91,6 +91,28 @@ def test_kernel_mask_windows_match_oracle_mask(by_key):
             np.testing.assert_array_equal(got, oracle.visibility_mask(L, S), err_msg=f"L={L} S={S}")
 
 
+@pytest.mark.parametrize("by_key", [False, True])
+def test_run_windows_are_the_union_of_row_masks(by_key):
+    """The per-wave windows the kernels skip 32-wide blocks with: for every run
+    of `group` consecutive rows of a half, exactly the keys (queries) that
+    some row of the run sees (is seen by) in the oracle's mask."""
+    for L in (1, 3, 8, 13, 31, 64, 100):
+        for S in sorted({1, 2, 3, 4, 5, 8, 32, L, L + 1}):
+            M = oracle.visibility_mask(L, S)
+            if by_key:
+                M = M.T  # rows: keys, columns: the queries that see them
+            for group in (1, 4, 32):
+                want = np.zeros_like(M)
+                for h in (0, 1):
+                    for r0 in range(0, L, group):
+                        rows = slice(h * L + r0, h * L + min(L, r0 + group))
+                        want[rows] = M[rows].any(axis=0)
+                got = bd.bd_attn_group_windows_host(L, S, by_key, group).astype(bool)
+                if by_key:
+                    got = got.T
+                np.testing.assert_array_equal(got, want, err_msg=f"L={L} S={S} group={group}")
+
+
 def test_classifier_tile_counts_8b_shape():
     # L=2048, S=4 with 128x128 tiles: per (b, h) 1024 pairs; 240 FULL, 48 PARTIAL, 736 EMPTY
     c = bd.bd_attn_classify_tiles_host(2048, 4, 128, 128)
