@@ -574,6 +574,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(lds_tr<D>(kcur, ops.tr_rel0, ops.tr_rel1, c, db), dsb[c], dqacc[db]);
+      // K^T operand reads four MFMAs ahead
+      pipeline_lds_reads<PC * DB, 4, 2>();
     }
   };
   // One 32-key block kb of a diagonal key tile (the next tile's copy is

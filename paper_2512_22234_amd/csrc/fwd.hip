@@ -150,10 +150,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   // cannot overwrite the tiles being read, so it does not wait for the copy
   // before the reads (the wait at the end of the step covers it).
   //
-  // The copy of the next tile is spread over the step: its K part between the
-  // score MFMAs, its V part between the PV MFMAs.  A CU accepts vector memory
-  // requests at a limited rate, so a burst of copies at the top of the step
-  // would stall the wave; spread out, each request issues while MFMAs run.
+  // The copy of the next tile (K and V) is spread between the score MFMAs,
+  // early enough in the step that the V part has landed by its end (issued
+  // between the PV MFMAs instead, it made the end-of-step wait 2% of the
+  // kernel).  A CU accepts vector memory requests at a limited rate, so a
+  // burst of copies at the top of the step would stall the wave; spread out,
+  // each request issues while MFMAs run.
   // The last step copies its own tile again (into the buffer nothing reads
   // afterwards), which keeps the step straight-line code.
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
@@ -171,8 +173,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(lds_rows<D>(kcur, ops.row_rel, s, kb), qreg[s], sacc[kb]);
       issue(tn, false, knxt);
-      // K operand reads four MFMAs ahead, the copy spread between the MFMAs
-      pipeline_reads_and_copies<DS * KB, 4, 1, decltype(copy)::NI>();
+      issue(tn, true, vnxt);
+      // K operand reads four MFMAs ahead, the copies spread between the MFMAs
+      pipeline_reads_and_copies<DS * KB, 4, 1, 2 * decltype(copy)::NI>();
       if (!full) {
         // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
         const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
@@ -226,8 +229,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       for (int c = 0; c < PC; ++c)
 #pragma unroll
         for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, c, db), pb[c], oacc[db]);
-      issue(tn, true, vnxt);
-      interleave_copies<PC * DB, decltype(copy)::NI>();
+      pipeline_lds_reads<PC * DB, 4, 2>();  // V^T operand reads (two per MFMA) four MFMAs ahead
     }
   };
   // One 32-key block kb of a key tile, for the diagonal tiles: the same
