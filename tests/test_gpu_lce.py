@@ -172,6 +172,36 @@ def test_lce_full_size_sampled():
     assert np.abs(col).max() <= 1e-2 * np.abs(_np(dw)).sum(0).max()
 
 
+def test_lce_full_size_kept_logits_match_recompute():
+    """The kept-logits variants at the full 8B LM-head shape (the forward that
+    also stores the float32 logits, and the backward that forms g from them):
+    LSE and logp are bitwise those of the plain forward, the kept logits of
+    sampled positions are H W^T, and the gradients agree with the recomputing
+    backward to the bf16 rounding of g."""
+    from paper_2512_22234_amd import bd_lce_logits_bytes
+    c = LCE_WORKLOADS["8b_lm_head"]
+    N, V, Dm = c["N"], c["V"], c["Dm"]
+    h, w, t = make_lce_inputs(N, V, Dm, seed=c["seed"], device="cuda")
+    dl = torch.randn(N, generator=torch.Generator(device="cuda").manual_seed(3), device=DEV) / N
+    keep = torch.empty(bd_lce_logits_bytes(N, V, Dm) // 4, dtype=torch.float32, device=DEV)
+    lse_k, logp_k = bd_lce_fwd(h, w, t, logits=keep)
+    lse, logp = bd_lce_fwd(h, w, t)
+    dh_k, dw_k = bd_lce_bwd(h, w, t, lse_k, dl, logits=keep)
+    dh, dw = bd_lce_bwd(h, w, t, lse, dl)
+    torch.cuda.synchronize()
+    assert torch.equal(lse_k, lse) and torch.equal(logp_k, logp)
+    rows = [0, 1, 2047, N - 1]
+    Vp = keep.numel() // N
+    kept = keep.view(N, Vp)[rows, :V].double().cpu().numpy()
+    want = h[rows].double().cpu().numpy() @ w.double().cpu().numpy().T
+    assert np.abs(kept - want).max() <= 1e-4 * max(1.0, np.abs(want).max())
+    assert np.all(keep.view(N, Vp)[rows, V:].cpu().numpy() == 0)  # the zero rows' logits
+    def rel(x, y):  # relative L2 on the device (the full gradients are large)
+        x, y = x.float(), y.float()
+        return float(torch.linalg.vector_norm(x - y) / torch.linalg.vector_norm(y))
+    assert rel(dh_k, dh) <= 2e-3 and rel(dw_k, dw) <= 2e-3
+
+
 def test_lce_invalid_arguments():
     h, w, t = (x.to(DEV) for x in make_lce_inputs(8, 300, 256, seed=5))
     assert bd_lce_workspace_bytes(8, 300, 200, 0) == 0           # Dm not a multiple of 256
