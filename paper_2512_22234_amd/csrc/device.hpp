@@ -229,21 +229,6 @@ __device__ inline void async_load_row_floats(const float* arr, int nrows, int ro
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)dst, 4, 4 * lane, 0, 0, 0);
 }
 
-// Scheduling request for the current basic block: spread NV vector-memory
-// instructions (tile copies) evenly between NM MFMAs instead of issuing them
-// as one burst.
-// Place it right after the copies, which follow the MFMAs in program order;
-// SYNC separates independent requests in one block.
-template <int NM, int NV, int SYNC = 0>
-__device__ inline void interleave_copies() {
-  static_assert(NV >= 1 && NM >= NV, "at least one MFMA per copy");
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, NM / NV, SYNC);  // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, SYNC);        // VMEM read
-  }
-}
-
 // Scheduling request for the current basic block of NM MFMAs that each take
 // RPM LDS operand reads and share NV copy instructions: the reads run AHEAD
 // MFMAs ahead of their use and the copies are spread evenly between the
