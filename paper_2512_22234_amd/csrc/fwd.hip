@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   const PosWindow uw_n = wave_keys_visible(qh, HALF_NOISY, wr0, wr1, L, S);
   const PosWindow uw_c = wave_keys_visible(qh, HALF_CLEAN, wr0, wr1, L, S);
 
-  // One key tile.  The current K/V tiles and the buffers the next tile is
+  // One FULL key tile.  The current K/V tiles and the buffers the next tile is
   // copied into are distinct restrict-qualified pointers: the alias scopes
   // this gives every LDS access let the compiler see that the copy in flight
   // cannot overwrite the tiles being read, so it does not wait for the copy
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   // The last step copies its own tile again (into the buffer nothing reads
   // afterwards), which keeps the step straight-line code.
   auto tile_step = [&](const char* __restrict__ kcur, const char* __restrict__ vcur, char* __restrict__ knxt,
-                       char* __restrict__ vnxt, int t, bool full, int kh, int k0) __attribute__((always_inline)) {
+                       char* __restrict__ vnxt, int t) __attribute__((always_inline)) {
     const int tn = imin(t + 1, T - 1);
     {
       f32x16 sacc[KB];
@@ -176,21 +176,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       issue(tn, true, vnxt);
       // K operand reads four MFMAs ahead, the copies spread between the MFMAs
       pipeline_reads_and_copies<DS * KB, 4, 1, 2 * decltype(copy)::NI>();
-      if (!full) {
-        // key k0 + offset of this tile is visible iff win.lo <= k0 + offset < win.hi
-        const PosWindow win = kh == HALF_NOISY ? win_n : win_c;
-        const unsigned span = (unsigned)(win.hi - win.lo);
-        const int rel = k0 + 4 * g2 - win.lo;
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-              const unsigned pos = (unsigned)(rel + kb * 32 + 8 * i + jj);
-              sacc[kb][4 * i + jj] = pos < span ? sacc[kb][4 * i + jj] : -INFINITY;
-            }
-      }
+      // (a FULL tile: every key is visible from every row, no test)
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
@@ -302,9 +288,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   for (int t = 0; t < t_main; ++t) {
     char *cur, *nxt;
     step_buffers(t, cur, nxt);
-    int kh, j;
-    kl.at(t, kh, j);
-    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t, true, kh, j * BN);
+    tile_step(cur, cur + 2 * TILE, nxt, nxt + 2 * TILE, t);
     end_step();
   }
   for (int t = t_main; t < T; ++t) {
