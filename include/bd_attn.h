@@ -116,7 +116,9 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
  * exactly once.  A visited pair whose class, as the kernels compute it
  * without divisions (and the two-comparison FULL test the kernels apply
  * per step), differs from bd_attn_classify_tiles_host's gets 64 instead
- * of 1.
+ * of 1; so does a key tile that the forward and dQ kernels would run in
+ * their leading loop of FULL tiles (no visibility test) without it being
+ * FULL.
  */
 int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out);
 

@@ -238,6 +238,8 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
       const int qA = (q0 / S) * S, qB = ((q1 - 1) / S) * S;
       const bd::FullRange fr = bd::full_range_vs_query_tile(qh, q0, q1, L, S, BM);
       const bd::KeyTileList kl = bd::key_tiles_for_query_tile(qh, a % nqt, L, S, BM, BN);
+      // the forward and dQ kernels run the first t_main tiles with no visibility test
+      const int t_main = bd::imin(kl.count(), fr.full_prefix(BN));
       for (int t = 0; t < kl.count(); ++t) {
         int kh, j;
         kl.at(t, kh, j);
@@ -246,7 +248,8 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
         const bool full = (q1 - q0) == BM && (k1 - k0) == BN;
         const int ref = bd::classify_pair(qh, q0, q1, kh, k0, k1, S, full);
         const int fast = bd::classify_vs_query_tile(qh, qA, qB, S, kh, k0, k1, full);
-        const bool ok = fast == ref && fr.full(kh, k0, BN) == (ref == bd::TILE_FULL);
+        const bool ok = fast == ref && fr.full(kh, k0, BN) == (ref == bd::TILE_FULL) &&
+                        (t >= t_main || ref == bd::TILE_FULL);
         out[(size_t)a * nk + kh * nkt + j] += (int8_t)(ok ? 1 : 64);
       }
     }

@@ -83,6 +83,18 @@ def test_tile_walks_visit_each_nonempty_pair_once(L, S, BM, BN):
         np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"by_key={by_key}")
 
 
+def test_forward_full_prefix_holds_only_full_tiles():
+    """The forward and dQ kernels run the leading key tiles of a query tile's
+    walk in a loop with no visibility test; the host twin marks a pair of
+    that prefix that is not FULL (and any other walk error) with 64.  Swept
+    over the kernels' own tiles (128 query rows, 64 keys)."""
+    for L in list(range(1, 70)) + [100, 127, 128, 129, 200, 255, 256, 257, 300, 513, 1000, 2048]:
+        for S in sorted({1, 2, 3, 4, 5, 7, 8, 16, 31, 32, 33, 64, 100, 128, 129, L, L + 1}):
+            visits = bd.bd_attn_visit_lists_host(L, S, 128, 64, False)
+            cls = bd.bd_attn_classify_tiles_host(L, S, 128, 64)
+            np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"L={L} S={S}")
+
+
 @pytest.mark.parametrize("by_key", [False, True])
 def test_kernel_mask_windows_match_oracle_mask(by_key):
     for L in (1, 2, 3, 5, 8, 13, 16, 31, 64):
