@@ -4,11 +4,12 @@
 One step = bd_attn_fwd + bd_attn_bwd over one batch of the 8B-shaped training
 workload (B=2, Hq=32, Hkv=8, D=128, L=2048 so 4096 packed tokens, S=4, bf16
 N(0,1)*0.5 inputs, dO ~ N(0,1)), inputs resident in HBM (warm caches: the
-working set fits the 256 MB Infinity Cache).  W untimed warm-up steps (100,
-about 75 ms: the GPU's clocks settle only after tens of milliseconds under
-load), then K timed steps (50) bracketed by device synchronisation and HIP
-events on the stream the library runs on; the per-step median is reported
-beside the mean.
+working set fits the 256 MB Infinity Cache).  First a clock-settle phase of
+untimed steps for a fixed wall time (250 ms by default, reported as
+`settle_ms`: the GPU's clocks settle only after tens of milliseconds under
+load), then W untimed warm-up steps (10), then K timed steps (50) bracketed
+by device synchronisation and HIP events on the stream the library runs on;
+the per-step median is reported beside the mean.
 
 value  = effective TFLOP/s counting only visible (query, key) pairs:
          (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
@@ -126,7 +127,7 @@ def cpu_baseline(w, budget_s: float, max_groups: int):
     q, k, v, do = make_inputs(w)
     G = w.Hq // w.Hkv
     groups = [(b, g) for b in range(w.B) for g in range(w.Hkv)]
-    done, t_total = 0, 0.0
+    done, t_fwd, t_bwd = 0, 0.0, 0.0
     for b, g in groups[:max_groups]:
         sl = slice(g * G, (g + 1) * G)
         Q = q[b:b + 1, sl].double().numpy()
@@ -135,17 +136,34 @@ def cpu_baseline(w, budget_s: float, max_groups: int):
         dO = do[b:b + 1, sl].double().numpy()
         t0 = time.perf_counter()
         oracle.forward(Q, K, V, w.L, w.S)
+        t1 = time.perf_counter()
         oracle.backward(dO, Q, K, V, w.L, w.S)
-        t_total += time.perf_counter() - t0
+        t2 = time.perf_counter()
+        t_fwd += t1 - t0
+        t_bwd += t2 - t1
         done += 1
-        log(f"[cpu] oracle group {done}: {t_total:.1f}s cumulative")
-        if t_total >= budget_s:
+        log(f"[cpu] oracle group {done}: fwd {t_fwd:.1f}s bwd {t_bwd:.1f}s cumulative")
+        if t_fwd + t_bwd >= budget_s:
             break
-    flops = 14 * w.D * visible_pairs(w.L, w.S) * G * done
+    t_total = t_fwd + t_bwd
+    npairs = visible_pairs(w.L, w.S) * G * done
+    flops = 14 * w.D * npairs
+    # the oracle materialises the mask and multiplies dense 2L x 2L matrices:
+    # forward Z = Q K^T and O = P V, backward dP, dQ, dK and dV, per query head
+    N = 2 * w.L
+    dense_fwd, dense_bwd = 4 * N * N * w.D * G * done, 8 * N * N * w.D * G * done
+    n_groups = w.B * w.Hkv
     return {"value": round(flops / t_total / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{done} GQA group(s) ({G} query heads + 1 KV head each) of the {w.name} workload, "
-                      f"fwd+bwd in fp64 numpy ({blas} BLAS), {t_total:.1f} s; same visible-pair FLOP count"}
+            "sample": f"{done} of {n_groups} GQA groups ({G} query heads + 1 KV head each) of the {w.name} "
+                      f"workload, fwd+bwd in fp64 numpy ({blas} BLAS), {t_total:.1f} s; value counts the same "
+                      f"visible-pair FLOPs as the GPU line; the full workload is extrapolated from this sample",
+            "fwd_s": round(t_fwd, 3), "bwd_s": round(t_bwd, 3),
+            "groups_timed": done, "groups_total": n_groups,
+            "full_workload_s_extrapolated": round(t_total * n_groups / done, 2),
+            "effective_gflop_sample": round(flops / 1e9, 3),
+            "dense_fp64_gflop_executed": {"fwd": round(dense_fwd / 1e9, 3), "bwd": round(dense_bwd / 1e9, 3)},
+            "dense_fp64_gflops_rate": round((dense_fwd + dense_bwd) / t_total / 1e9, 2)}
 
 
 def packed_step(steps: int, warmup: int, name: str = "8b_packed"):
@@ -305,7 +323,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--settle-ms", type=float, default=250.0,
+                    help="wall time of untimed steps before the warm-up, for the clocks to settle (0: none)")
     ap.add_argument("--workload", default="8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-packed", action="store_true", help="skip the packed-sequence measurement")
@@ -363,7 +383,18 @@ def main():
             bd.bd_attn_fwd_marked(q, k, v, L, S, fwd_marks[i], out=o, lse=lse, workspace=wsf)
             bd.bd_attn_bwd_marked(do, q, k, v, o, lse, L, S, bwd_marks[i], dq=dq, dk=dk, dv=dv, workspace=wsb)
 
-    log(f"[bench] {w.describe()}: warmup {args.warmup}, timed {K} steps")
+    # Clock settle: the GPU's clocks settle only after tens of milliseconds of
+    # sustained load, so before the W warm-up steps the step runs for a fixed
+    # wall time (reported as its own field; 0 disables it).
+    settle_steps, t_settle = 0, time.perf_counter()
+    while args.settle_ms > 0 and (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        settle_steps += 10
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t_settle) * 1e3 if settle_steps else 0.0
+    log(f"[bench] {w.describe()}: clock settle {settle_ms:.0f} ms ({settle_steps} steps), warmup {args.warmup}, "
+        f"timed {K} steps")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -430,6 +461,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "pct_of_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 3),
+        "settle_ms": round(settle_ms, 1), "settle_steps": settle_steps,
         "config": {"workload": f"{w.name}: B={w.B} Hq={w.Hq} Hkv={w.Hkv} D={w.D} L={L} (packed {2 * L}) "
                                f"S={S}, bf16 N(0,1)*0.5, fwd+bwd",
                    "global_batch": w.B, "seq_len": 2 * L, "parallelism": "single GPU",

@@ -80,7 +80,13 @@ int bd_attn_fwd(const void* Q, const void* K, const void* V,
  * Backward pass: the vector-Jacobian product of the forward pass for the
  * upstream gradient dO, given the forward's O and LSE.  Writes dQ, dK, dV
  * (dK and dV summed over the Hq/Hkv query heads sharing each KV head).
- * Deterministic: no atomics, results are bitwise reproducible.
+ * Deterministic: no floating-point atomics, so results are bitwise
+ * reproducible.  The only atomic is one integer arrival counter per group of
+ * 32 keys of each clean key tile, with which the two workgroups that split
+ * that tile's query walk decide which of them adds the other's float32 sums
+ * (the sum is the same either way).  Should that meeting ever fail to
+ * complete within its bounded wait, the affected dK/dV rows are written as
+ * NaN rather than as a partial sum.
  * ws/ws_bytes: at least bd_attn_workspace_bytes(..., for_bwd = 1) bytes.
  */
 int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,

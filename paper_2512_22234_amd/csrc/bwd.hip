@@ -365,11 +365,30 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       }
       // Bounded wait (the first half is past its last step and only stores
       // its sums); the bound only guarantees that the wave always ends.
+      int seen = 0;
       for (int spin = 0; spin < (1 << 22); ++spin) {
-        if (__hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+        seen = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (seen != 0) break;
         __builtin_amdgcn_s_sleep(2);
       }
       asm volatile("" ::: "memory");
+      if (seen == 0) {
+        // The other half's sums were never published: the result would be
+        // wrong, so this wave's keys get NaN instead of a plausible value.
+        const float nan = __builtin_nanf("");
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int key = kc0 + 32 * ks + l32;
+          if (key < k1) {
+            bf16* op = outp + (orow + key) * D + 4 * g2;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) st_bf16x4(op + db * 32 + 8 * i, nan, nan, nan, nan);
+          }
+        }
+        return;
+      }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const int key = kc0 + 32 * ks + l32;

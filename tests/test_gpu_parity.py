@@ -6,9 +6,10 @@ rel-L2 <= 5e-3, LSE max-abs <= 1e-3, dQ/dK/dV rel-L2 <= 1e-2 each.  The
 oracle sees the exact bf16 values the kernels see (float32 inputs are
 rounded to bf16 first, as the library does).
 
-Small and medium shapes are compared element by element in full; the 8B and
-block-size-sweep shapes on whole GQA groups; the long shape on sampled query
-rows and key rows, each evaluated exactly by the oracle.
+Small and medium shapes are compared element by element in full; the 8B
+shape on every GQA group (all of its outputs); the block-size-sweep shapes on
+two whole GQA groups each; the long shape on sampled query rows and key rows,
+each evaluated exactly by the oracle.
 """
 import numpy as np
 import pytest
@@ -110,13 +111,18 @@ def test_small_config_full():
     check_full(q, k, v, do, w.L, w.S, label="small")
 
 
-def test_8b_config_groups():
-    check_groups(WORKLOADS["8b"], [(0, 0), (1, 7)], "8b")
+@pytest.mark.parametrize("b", [0, 1])
+def test_8b_config_all_groups(b):
+    """Every (batch, KV head) group of the 8B workload, element by element:
+    one batch entry (8 groups, 32 query heads) per test."""
+    w = WORKLOADS["8b"]
+    check_groups(w, [(b, g) for g in range(w.Hkv)], "8b")
 
 
 @pytest.mark.parametrize("name", ["8b_s8", "8b_s16", "8b_s32", "8b_s64"])
 def test_block_size_sweep_groups(name):
-    check_groups(WORKLOADS[name], [(1, 3)], name)
+    # the first and the last group of the batch (XCD remap and both batch entries)
+    check_groups(WORKLOADS[name], [(0, 0), (1, 7)], name)
 
 
 def test_long_config_sampled():

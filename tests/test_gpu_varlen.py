@@ -119,3 +119,32 @@ def test_varlen_invalid_arguments_raise():
     with pytest.raises(BdAttnError) as e:
         bd_attn_varlen_fwd(q, k, v, cu, 20, 0)      # S < 1
     assert e.value.status == 1
+
+
+def test_varlen_measured_packed_workload():
+    """The packed workload the benchmark measures (the 8B heads, 4096 tokens per
+    copy split into six sequences of 130..1701 tokens), every output compared:
+    each sequence of each GQA group against the single-sequence oracle on that
+    sequence's rows (the packed oracle equals it sequence by sequence)."""
+    from paper_2512_22234_amd.workloads import VARLEN_WORKLOADS, varlen_lengths
+    c = VARLEN_WORKLOADS["8b_packed"]
+    lengths = varlen_lengths(c["total"], c["seed"], c["lo"], c["hi"])
+    Hq, Hkv, D, S = c["Hq"], c["Hkv"], c["D"], c["S"]
+    print(f"[varlen] 8b_packed lengths={lengths} H{Hq}/{Hkv} D{D} S{S}", flush=True)
+    q, k, v, do, cu = make_varlen_inputs(lengths, Hq, Hkv, D, c["seed"])
+    o, lse, dq, dk, dv = (_np(t) for t in run_varlen(q, k, v, do, cu, max(lengths), S))
+    Q, K, V, dO = (t.double().numpy() for t in (q, k, v, do))
+    for i, Li in enumerate(lengths):
+        r0, r1 = 2 * int(cu[i]), 2 * int(cu[i + 1])
+        one = lambda x: x[None, :, r0:r1]  # [1, H, 2 Li, D]: the sequence as a batch of one
+        Or, LSEr = oracle.forward(one(Q), one(K), one(V), Li, S)
+        dQr, dKr, dVr = oracle.backward(one(dO), one(Q), one(K), one(V), Li, S)
+        errs = dict(o_max=float(np.abs(one(o) - Or).max()), o_rel=_rel(one(o), Or),
+                    lse_max=float(np.abs(lse[None, :, r0:r1] - LSEr).max()),
+                    dq_rel=max(_rel(one(dq)[:, h], dQr[:, h]) for h in range(Hq)),
+                    dk_rel=max(_rel(one(dk)[:, g], dKr[:, g]) for g in range(Hkv)),
+                    dv_rel=max(_rel(one(dv)[:, g], dVr[:, g]) for g in range(Hkv)))
+        print(f"[varlen] 8b_packed sequence {i} (L={Li}) errors {errs}", flush=True)
+        assert errs["o_max"] <= O_MAX and errs["o_rel"] <= O_REL, errs
+        assert errs["lse_max"] <= LSE_MAX, errs
+        assert max(errs["dq_rel"], errs["dk_rel"], errs["dv_rel"]) <= G_REL, errs
