@@ -33,8 +33,9 @@
  * `stream` in order and the call returns without waiting.  Outputs must not
  * overlap inputs.  The workspace may be reused once the enqueued work has
  * completed (stream order guarantees this for calls on the same stream).
- * The library keeps no mutable global state; calls from several host threads
- * are safe.
+ * Apart from the scratch array of bd_attn_bwd_noalloc (and the per-device
+ * address of it, looked up once under a lock), the library keeps no mutable
+ * global state; calls from several host threads are safe.
  *
  * Errors: every entry point validates its arguments before enqueuing
  * anything; a call that returns non-zero has enqueued no work (except
@@ -57,7 +58,8 @@ enum bd_attn_status {
   BD_ATTN_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, B,L,S<1, L>2^22, Hq%Hkv!=0, overlap */
   BD_ATTN_ERR_UNSUPPORTED = 2,      /* D not in {64,128}, unknown dtype */
   BD_ATTN_ERR_WORKSPACE_TOO_SMALL = 3, /* checked before overlap with the workspace */
-  BD_ATTN_ERR_HIP = 4               /* a HIP launch reported an error */
+  BD_ATTN_ERR_HIP = 4,              /* a HIP launch reported an error */
+  BD_ATTN_ERR_EXCEEDS_SCRATCH = 5   /* bd_attn_bwd_noalloc: the problem needs more than its scratch */
 };
 
 enum bd_attn_dtype { BD_ATTN_BF16 = 0, BD_ATTN_FP32 = 1 };
@@ -93,6 +95,29 @@ int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
                 const void* O, const float* LSE,
                 int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
                 void* dQ, void* dK, void* dV, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * bd_attn_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, work, results (bitwise) and
+ * validation as bd_attn_bwd; the workspace is a fixed device array inside the
+ * library of BD_ATTN_NOALLOC_SCRATCH_BYTES bytes, one per GPU, held from the
+ * library's first use on that GPU until the process ends.  A problem whose
+ * bd_attn_workspace_bytes(..., for_bwd = 1) exceeds it is rejected with
+ * BD_ATTN_ERR_EXCEEDS_SCRATCH before anything is enqueued (in bfloat16 the
+ * workspace is B*Hq*2L*8 + B*Hkv*L*D*8 bytes plus a few KiB: 34.0 MiB for
+ * B=2, Hq=32, Hkv=8, D=128, L=2048 and 68.0 MiB for B=1, L=8192 at the same
+ * heads; float32 inputs also need bf16 copies of every tensor).  The call
+ * allocates and frees nothing; its first call on a GPU looks up that GPU's
+ * copy of the array.  All calls on one GPU share the array and leave their
+ * contents in it: calls whose work may overlap in time on one GPU (other
+ * streams, other host threads) race and must be serialised by the caller.
+ */
+#define BD_ATTN_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+int bd_attn_bwd_noalloc(const void* dO, const void* Q, const void* K, const void* V,
+                        const void* O, const float* LSE,
+                        int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                        void* dQ, void* dK, void* dV, hipStream_t stream);
 
 /*
  * Workspace bytes needed by bd_attn_fwd (for_bwd = 0) or bd_attn_bwd

@@ -25,7 +25,7 @@ BD_ATTN_FP32 = 1
 __all__ = [
     "bd_attn", "BdAttnFunction", "bd_attn_fwd", "bd_attn_bwd", "bd_attn_workspace_bytes",
     "bd_attn_classify_tiles_host", "bd_attn_visit_lists_host", "bd_attn_mask_windows_host",
-    "bd_attn_status_string",
+    "bd_attn_status_string", "bd_attn_bwd_noalloc", "BD_ATTN_NOALLOC_SCRATCH_BYTES",
     "bd_attn_version", "bd_attn_fwd_marked", "bd_attn_bwd_marked", "bd_attn_stage_names",
     "BdAttnError", "BD_ATTN_BF16", "BD_ATTN_FP32",
     "bd_attn_varlen", "BdAttnVarlenFunction", "bd_attn_varlen_fwd", "bd_attn_varlen_bwd",
@@ -206,6 +206,29 @@ def bd_attn_bwd(do, q, k, v, o, lse, L: int, S: int, scale=None, dq=None, dk=Non
     if stream is not None and workspace is None:
         ws.record_stream(s)
     return dq_, dk_, dv_
+
+
+BD_ATTN_NOALLOC_SCRATCH_BYTES = 96 << 20   # the library's scratch array for bd_attn_bwd_noalloc
+
+
+def bd_attn_bwd_noalloc(do, q, k, v, o, lse, L: int, S: int, dq, dk, dv, scale=None, stream=None):
+    """bd_attn_bwd with the library's own scratch array as its workspace (for
+    callers that cannot allocate): writes the caller's dq, dk, dv and returns
+    them.  Calls whose work overlaps in time on one GPU race on that array."""
+    B, Hq, Hkv, D = _shapes(q, k, L)
+    dev, dt = q.device, q.dtype
+    code = _dtype_code(q)
+    for name, t, shp in (("do", do, q.shape), ("q", q, q.shape), ("k", k, (B, Hkv, 2 * L, D)),
+                         ("v", v, (B, Hkv, 2 * L, D)), ("o", o, q.shape), ("dq", dq, q.shape),
+                         ("dk", dk, (B, Hkv, 2 * L, D)), ("dv", dv, (B, Hkv, 2 * L, D))):
+        _check(name, t, shp, dt, dev)
+    _check("lse", lse, (B, Hq, 2 * L), torch.float32, dev)
+    _, sh = _stream(dev, stream)
+    st = lib().bd_attn_bwd_noalloc(_ptr(do), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, S, Hq, Hkv, D,
+                                   _scale_arg(scale), code, _ptr(dq), _ptr(dk), _ptr(dv), sh)
+    if st:
+        raise BdAttnError(st, "bd_attn_bwd_noalloc")
+    return dq, dk, dv
 
 
 class BdAttnFunction(torch.autograd.Function):

@@ -36,6 +36,8 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_bwd.restype = ci
     L.bd_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci,
                               vp, vp, vp, vp, sz, vp]
+    L.bd_attn_bwd_noalloc.restype = ci
+    L.bd_attn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci, vp, vp, vp, vp]
     L.bd_attn_fwd_marked.restype = ci
     L.bd_attn_fwd_marked.argtypes = L.bd_attn_fwd.argtypes + [vp, ci]
     L.bd_attn_bwd_marked.restype = ci

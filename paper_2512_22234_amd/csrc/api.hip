@@ -5,10 +5,19 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "bd_attn.h"
 #include "kernels.hpp"
 #include "tiles.hpp"
+
+// Device memory of bd_attn_bwd_noalloc: the backward's workspace (per query
+// row (lse2, Delta), the float32 sums of split key-tile walks and their
+// pairing counters) for callers that cannot allocate.  Every GPU that runs a
+// kernel of this library holds one copy until the process ends.  In host code
+// the name stands for a host-side shadow, not a device address: only the
+// per-device address from hipGetSymbolAddress may be handed to kernels.
+static __device__ __align__(256) char scratch[BD_ATTN_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -170,6 +179,32 @@ struct Marks {
   }
 };
 
+// Device address of `scratch` on the device that runs `stream` (the current
+// device for the null stream), looked up on the first call for that device
+// with the device current.  Returns a status.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_for_stream(hipStream_t stream, void** out) {
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return BD_ATTN_ERR_HIP;
+  int dev = cur;
+  if (stream != nullptr && hipStreamGetDevice(stream, &dev) != hipSuccess) return BD_ATTN_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return BD_ATTN_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return BD_ATTN_ERR_HIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur && hipSetDevice(cur) != hipSuccess) return BD_ATTN_ERR_HIP;
+    if (e != hipSuccess || p == nullptr) return BD_ATTN_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BD_ATTN_OK;
+}
+
 // Work of one call on a validated shape.
 int fwd_impl(const bd::Shape& s, const void* Q, const void* K, const void* V, int dtype, void* O, float* LSE,
              void* ws, size_t ws_bytes, hipStream_t stream, Marks marks);
@@ -190,6 +225,8 @@ const char* bd_attn_status_string(int status) {
     case BD_ATTN_ERR_UNSUPPORTED: return "unsupported head dimension or dtype";
     case BD_ATTN_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
     case BD_ATTN_ERR_HIP: return "HIP launch error";
+    case BD_ATTN_ERR_EXCEEDS_SCRATCH:
+      return "problem needs more workspace than the no-allocation entry point's scratch holds";
     default: return "unknown status";
   }
 }
@@ -358,6 +395,25 @@ int bd_attn_bwd_marked(const void* dO, const void* Q, const void* K, const void*
   const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
   if (st != BD_ATTN_OK) return st;
   return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, ws_bytes, stream, Marks{marks, n_marks});
+}
+
+int bd_attn_bwd_noalloc(const void* dO, const void* Q, const void* K, const void* V, const void* O,
+                        const float* LSE, int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,
+                        void* dQ, void* dK, void* dV, hipStream_t stream) {
+  bd::Shape s;
+  const int st = validate(B, L, S, Hq, Hkv, D, scale, dtype, s);
+  if (st != BD_ATTN_OK) return st;
+  if (make_layout(s, dtype, true).total > (size_t)BD_ATTN_NOALLOC_SCRATCH_BYTES) return BD_ATTN_ERR_EXCEEDS_SCRATCH;
+  // the argument checks that need no workspace, before the first HIP call
+  if (!dO || !Q || !K || !V || !O || !LSE || !dQ || !dK || !dV) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (!aligned(dO, 16) || !aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+      !aligned(LSE, 4) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16))
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
+  void* ws = nullptr;
+  const int sst = scratch_for_stream(stream, &ws);
+  if (sst != BD_ATTN_OK) return sst;
+  return bwd_impl(s, dO, Q, K, V, O, LSE, dtype, dQ, dK, dV, ws, (size_t)BD_ATTN_NOALLOC_SCRATCH_BYTES, stream,
+                  Marks{nullptr, 0});
 }
 
 int bd_attn_varlen_fwd(const void* Q, const void* K, const void* V, const int32_t* cu_seqlens, int n_seqs,

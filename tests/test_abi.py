@@ -29,11 +29,11 @@ def test_library_exports_every_declared_symbol():
 def test_version_and_status_strings():
     assert bd.bd_attn_version() == 100
     seen = set()
-    for st in range(5):
+    for st in range(6):
         s = bd.bd_attn_status_string(st)
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == 5
+    assert len(seen) == 6
     assert bd.bd_attn_status_string(99) == "unknown status"
 
 
@@ -318,3 +318,34 @@ def test_lce_objective_validation(kind, eps, beta, old, adv, ref, status):
     st = _lib.lib().bd_lce_objective(p(0), p(1, old), p(2, ref), p(3, adv), p(4), 8, kind, eps, beta, p(5), p(6),
                                      vp(None))
     assert st == status
+
+
+def _bwd_noalloc(**kw):
+    a = dict(dO=A, Q=A + SZ, K=A + 2 * SZ, V=A + 3 * SZ, O=A + 4 * SZ, LSE=A + 5 * SZ, B=1, L=64, S=4,
+             Hq=2, Hkv=1, D=64, scale=0.0, dtype=0, dQ=A + 6 * SZ, dK=A + 7 * SZ, dV=A + 8 * SZ, stream=None)
+    a.update(kw)
+    vp = ctypes.c_void_p
+    return _lib.lib().bd_attn_bwd_noalloc(vp(a["dO"]), vp(a["Q"]), vp(a["K"]), vp(a["V"]), vp(a["O"]),
+                                          vp(a["LSE"]), a["B"], a["L"], a["S"], a["Hq"], a["Hkv"], a["D"],
+                                          a["scale"], a["dtype"], vp(a["dQ"]), vp(a["dK"]), vp(a["dV"]),
+                                          vp(a["stream"]))
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define BD_ATTN_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == bd.BD_ATTN_NOALLOC_SCRATCH_BYTES
+    # the long workload's bf16 backward fits, its float32 variant does not
+    assert bd.bd_attn_workspace_bytes(1, 8192, 4, 32, 8, 128, 0, 1) <= bd.BD_ATTN_NOALLOC_SCRATCH_BYTES
+    assert bd.bd_attn_workspace_bytes(1, 8192, 4, 32, 8, 128, 1, 1) > bd.BD_ATTN_NOALLOC_SCRATCH_BYTES
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=96), 2), (dict(dtype=3), 2), (dict(Hq=3, Hkv=2), 1), (dict(B=0), 1), (dict(L=0), 1),
+    (dict(L=(1 << 22) + 1), 1),
+    # workspace beyond the scratch array: rejected before any HIP call
+    (dict(B=4, L=8192, Hq=32, Hkv=8, D=128), 5), (dict(B=1, L=8192, Hq=32, Hkv=8, D=128, dtype=1), 5),
+    (dict(dO=0), 1), (dict(dV=0), 1), (dict(LSE=A + 5 * SZ + 2), 1), (dict(dK=A + 7 * SZ + 4), 1),
+])
+def test_bwd_noalloc_validation(kw, status):
+    assert _bwd_noalloc(**kw) == status
