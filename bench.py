@@ -17,6 +17,11 @@ value  = effective TFLOP/s counting only visible (query, key) pairs:
 roofline: the dominant kernel's algorithmic FLOPs per launch over its average
          duration, from events recorded around every kernel launch of the timed
          steps, against the bf16 dense MFMA peak.
+kernels: per kernel the event-timed duration and algorithmic rate, and, from
+         the committed rocprofv3 counter record of the same kernel sources
+         (profiles/bd_attn_8b_counters.md), the executed MFMA rate over this
+         run's duration, the MFMA and LDS busy fractions the counters showed and
+         the HBM bytes per launch and GB/s.
 cpu_baseline: the fp64 oracle (test infrastructure) timed on the host cores on
          a bounded sample of the same workload (whole GQA groups).
 packed:  the same step over packed sequences of mixed lengths (the same heads,
@@ -65,7 +70,7 @@ def log(msg: str):
 
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-COUNTERS_FILE = os.path.join(HERE, "profiles", "bd_attn_8b_hbm_traffic.md")
+COUNTERS_FILE = os.path.join(HERE, "profiles", "bd_attn_8b_counters.md")
 
 
 def kernel_source_hash() -> str:
@@ -81,10 +86,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or
-    None when there is none for this workload or the kernel sources changed
-    since the counters were taken (the summary records the source hash)."""
+def counter_record(kernel: str, workload: str):
+    """The committed rocprofv3 counter figures of `kernel` (per launch), or None
+    when there are none for this workload or the kernel sources changed since
+    the counters were taken (the summary records the source hash)."""
     try:
         text = open(COUNTERS_FILE).read()
     except OSError:
@@ -95,7 +100,12 @@ def measured_traffic(kernel: str, workload: str):
     rec = json.loads(text[start + 7:text.index("```", start + 7)])
     if rec.get("source_sha256") != kernel_source_hash() or rec.get("workload") != workload:
         return None
-    k = rec.get("kernels", {}).get(kernel)
+    return rec.get("kernels", {}).get(kernel)
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None."""
+    k = counter_record(kernel, workload)
     return None if k is None else int(k["hbm_bytes_per_launch"])
 
 
@@ -432,6 +442,14 @@ def main():
         if name in alg:
             entry["tflops"] = round(alg[name] / (t * 1e-3) / 1e12, 2)
             entry["frac_of_peak"] = round(entry["tflops"] / PEAK_BF16_TFLOPS, 4)
+        # counter-derived figures (committed rocprofv3 record of these sources), over this run's timing
+        rec = counter_record(name, w.name)
+        if rec is not None:
+            entry["executed_mfma_tflops"] = round(rec["sq_insts_mfma"] * 32768 / (t * 1e-3) / 1e12, 1)
+            entry["mfma_busy_frac"] = rec["mfma_busy_frac"]
+            entry["lds_busy_frac"] = rec["lds_busy_frac"]
+            entry["hbm_bytes"] = rec["hbm_bytes_per_launch"]
+            entry["hbm_gbs"] = round(rec["hbm_bytes_per_launch"] / (t * 1e-3) / 1e9, 1)
         kernels[name] = entry
     dom = max(alg, key=lambda n: per[n])
     ach = alg[dom] / (per[dom] * 1e-3) / 1e12
