@@ -102,22 +102,27 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int kg = w & 3;  // key group
   const int l32 = lane & 31, g2 = lane >> 5;
 
-  // Items: clean key tiles in ascending index (most work first), each as two
-  // halves of its walk; then noisy key tiles, one item each.  Consecutive
-  // workgroups are different KV heads.
+  // Items: clean key tiles, most work first, each as two halves of its walk;
+  // then noisy key tiles, one item each.  Consecutive workgroups are
+  // different KV heads (or sequences).  A clean key tile at k0 is seen by
+  // about 2 (L - k0) queries, so the work of a tile is set by how many tiles
+  // of its sequence follow it: item rank r goes to the tile with nKT - r
+  // tiles from it to its sequence's end (nKT: the tile count of the longest
+  // sequence), which is tile r itself when every sequence has the maximum
+  // length.
   const int id = blockIdx.x;
   const int rank = id / p.nkv;
   const int grp = id - rank * p.nkv;  // b * Hkv + hk
   const bool clean = rank < 2 * p.nKT;
   const int kh = clean ? HALF_CLEAN : HALF_NOISY;
-  const int j = clean ? (rank >> 1) : rank - 2 * p.nKT;
   const int split = clean ? (rank & 1) : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
   // sequence b: its length and where its rows lie
   int L;
   size_t qrow0, krow0, hrows;
   p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
-  if (j * BN >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
+  const int j = clean ? (rank >> 1) - (p.nKT - cdiv(L, BN)) : rank - 2 * p.nKT;
+  if (j < 0 || j * BN >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
   // (a sequence shorter than S is one block: every formula below gives
   // the S = L mask then)
   const int S = p.S;
