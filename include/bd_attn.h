@@ -89,12 +89,14 @@ int bd_attn_fwd(const void* Q, const void* K, const void* V,
  * upstream gradient dO, given the forward's O and LSE.  Writes dQ, dK, dV
  * (dK and dV summed over the Hq/Hkv query heads sharing each KV head).
  * Deterministic: no floating-point atomics, so results are bitwise
- * reproducible.  The only atomic is one integer arrival counter per group of
- * 32 keys of each clean key tile, with which the two workgroups that split
- * that tile's query walk decide which of them adds the other's float32 sums
- * (the sum is the same either way).  Should that meeting ever fail to
- * complete within its bounded wait, the affected dK/dV rows are written as
- * NaN rather than as a partial sum.
+ * reproducible.  The only atomics are integer counters per group of 32 keys
+ * of each clean key tile (arrivals and published parts), with which the
+ * workgroups that split that tile's query walk (two, or four for shapes with
+ * few KV heads x length) decide which of them adds the others' float32 sums;
+ * the sums are added in part order, so the result is the same whichever part
+ * finishes last.  Should that meeting ever fail to complete within its
+ * bounded wait, the affected dK/dV rows are written as NaN rather than as a
+ * partial sum.
  * ws/ws_bytes: at least bd_attn_workspace_bytes(..., for_bwd = 1) bytes.
  */
 int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
@@ -111,9 +113,11 @@ int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
  * library's first use on that GPU until the process ends.  A problem whose
  * bd_attn_workspace_bytes(..., for_bwd = 1) exceeds it is rejected with
  * BD_ATTN_ERR_EXCEEDS_SCRATCH before anything is enqueued (in bfloat16 the
- * workspace is B*Hq*2L*8 + B*Hkv*L*D*8 bytes plus a few KiB: 34.0 MiB for
- * B=2, Hq=32, Hkv=8, D=128, L=2048 and 68.0 MiB for B=1, L=8192 at the same
- * heads; float32 inputs also need bf16 copies of every tensor).  The call
+ * workspace is B*Hq*2L*8 + (n-1)*B*Hkv*L*D*8 bytes plus a few KiB, where n is
+ * the number of parts each clean key tile's dK/dV walk is split into: 4 when
+ * B*Hkv*(L+128) <= 21845, else 2; 34.0 MiB for B=2, Hq=32, Hkv=8, D=128,
+ * L=2048 and 68.0 MiB for B=1, L=8192 at the same heads; float32 inputs also
+ * need bf16 copies of every tensor).  The call
  * allocates and frees nothing; its first call on a GPU looks up that GPU's
  * copy of the array.  All calls on one GPU share the array and leave their
  * contents in it: calls whose work may overlap in time on one GPU (other
@@ -149,7 +153,9 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
  * (query tile, key tile) pair, how many times the kernels visit it: walking
  * key tiles per query tile (forward and dQ, by_key_tile = 0) or query tiles
  * per key tile (dK/dV, by_key_tile = 1; that kernel repeats the walk for each
- * query head of the group).  A correct walk visits every non-EMPTY pair
+ * query head of the group, and splits each clean key tile's walk into nsplit
+ * parts, 2 or 4; nsplit is ignored for by_key_tile = 0, and any other value
+ * with by_key_tile = 1 is BD_ATTN_ERR_INVALID_ARGUMENT).  A correct walk visits every non-EMPTY pair
  * exactly once.  A visited pair whose class, as the kernels compute it
  * without divisions (and the two-comparison FULL test the kernels apply
  * per step), differs from bd_attn_classify_tiles_host's gets 64 instead
@@ -157,7 +163,7 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out);
  * their leading loop of FULL tiles (no visibility test) without it being
  * FULL.
  */
-int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out);
+int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int nsplit, int8_t* out);
 
 /*
  * Host-side copy of the per-element visibility rule of PARTIAL tiles

@@ -88,10 +88,10 @@ def bd_attn_classify_tiles_host(L: int, S: int, BM: int, BN: int) -> np.ndarray:
     return out
 
 
-def bd_attn_visit_lists_host(L: int, S: int, BM: int, BN: int, by_key_tile: bool) -> np.ndarray:
+def bd_attn_visit_lists_host(L: int, S: int, BM: int, BN: int, by_key_tile: bool, nsplit: int = 2) -> np.ndarray:
     nq, nk = 2 * (-(-L // BM)), 2 * (-(-L // BN))
     out = np.zeros((nq, nk), dtype=np.int8)
-    st = lib().bd_attn_visit_lists_host(L, S, BM, BN, int(by_key_tile), out.ctypes.data_as(ctypes.c_void_p))
+    st = lib().bd_attn_visit_lists_host(L, S, BM, BN, int(by_key_tile), nsplit, out.ctypes.data_as(ctypes.c_void_p))
     if st:
         raise BdAttnError(st, "bd_attn_visit_lists_host")
     return out

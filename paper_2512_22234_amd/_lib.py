@@ -70,7 +70,7 @@ def lib() -> ctypes.CDLL:
     L.bd_attn_classify_tiles_host.restype = ci
     L.bd_attn_classify_tiles_host.argtypes = [ci, ci, ci, ci, vp]
     L.bd_attn_visit_lists_host.restype = ci
-    L.bd_attn_visit_lists_host.argtypes = [ci, ci, ci, ci, ci, vp]
+    L.bd_attn_visit_lists_host.argtypes = [ci, ci, ci, ci, ci, ci, vp]
     L.bd_attn_mask_windows_host.restype = ci
     L.bd_attn_mask_windows_host.argtypes = [ci, ci, ci, vp]
     L.bd_attn_group_windows_host.restype = ci

@@ -82,6 +82,9 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // Common validation; fills the resolved shape (fixed-length layout).
 int validate(int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype, bd::Shape& s) {
   if (!shape_ok(B, L, S, Hq, Hkv)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  // the pairing counters of the dK/dV kernel (and its grid) are indexed with 32-bit integers
+  if ((size_t)bd::DKV_PAIR_INTS * 4 * B * Hkv * bd::cdiv(L, bd::DKV_BN) > (size_t)INT32_MAX)
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (D != 64 && D != 128) return BD_ATTN_ERR_UNSUPPORTED;
   if (dtype != BD_ATTN_BF16 && dtype != BD_ATTN_FP32) return BD_ATTN_ERR_UNSUPPORTED;
@@ -106,7 +109,8 @@ int validate_varlen(const int32_t* cu, int n_seqs, int total_L, int max_L, int S
       Hq % Hkv != 0)
     return BD_ATTN_ERR_INVALID_ARGUMENT;
   // the pairing counters of the dK/dV kernel are indexed with 32-bit integers
-  if ((size_t)8 * n_seqs * Hkv * bd::cdiv(max_L, bd::DKV_BN) > (size_t)INT32_MAX) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if ((size_t)bd::DKV_PAIR_INTS * 4 * n_seqs * Hkv * bd::cdiv(max_L, bd::DKV_BN) > (size_t)INT32_MAX)
+    return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (total_L > INT32_MAX / 2) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (cu == nullptr || !aligned(cu, 4)) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (std::isnan(scale) || std::isinf(scale)) return BD_ATTN_ERR_INVALID_ARGUMENT;
@@ -263,8 +267,9 @@ int bd_attn_classify_tiles_host(int L, int S, int BM, int BN, int8_t* out) {
   return BD_ATTN_OK;
 }
 
-int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8_t* out) {
+int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int nsplit, int8_t* out) {
   if (L < 1 || S < 1 || BM < 1 || BN < 1 || out == nullptr) return BD_ATTN_ERR_INVALID_ARGUMENT;
+  if (by_key_tile && nsplit != 2 && nsplit != 4) return BD_ATTN_ERR_INVALID_ARGUMENT;
   if (S > L) S = L;
   const int nqt = bd::cdiv(L, BM), nkt = bd::cdiv(L, BN);
   const int nq = 2 * nqt, nk = 2 * nkt;
@@ -298,8 +303,8 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int8
       // the walks of the workgroups that own this key tile, as the kernel
       // takes them (one query head: the kernel repeats each (tile, half)
       // once per head of the group)
-      for (int split = 0; split < 2; ++split) {
-        const bd::QueryWalk wk = bd::query_walk(kh, j, split, L, S, BM, BN, 1);
+      for (int split = 0; split < nsplit; ++split) {
+        const bd::QueryWalk wk = bd::query_walk(kh, j, split, nsplit, L, S, BM, BN, 1);
         bd::WalkPos pos = wk.first(), prev = pos;
         for (int t = 0; t < wk.steps(); ++t, pos.next(wk)) {
           prev = pos;

@@ -18,10 +18,11 @@
 // and dV and accumulate dV^T = dO^T P and dK^T = Q^T dS, whose A operands come
 // from the Q and dO tiles through the transposing LDS read.  Work per clean
 // key tile shrinks linearly with its position, so each clean tile's walk is
-// split into two halves run by two workgroups.  Whichever half finishes first
-// leaves its float32 sums in the workspace; the other adds them to its own and
-// writes dK/dV.  Float addition of two terms commutes, so the result does not
-// depend on which half finishes first.  Noisy key tiles (seen only by their
+// split into parts (two, or four when the heaviest half-walk would outlast the
+// average work of a CU) run by as many workgroups.  Every part but the last to
+// finish leaves its float32 sums in the workspace; the last adds all of them,
+// its own included, in part order and writes dK/dV, so the result does not
+// depend on which part finishes when.  Noisy key tiles (seen only by their
 // own block's noisy queries) are done by one workgroup each.
 //
 // dq: a workgroup owns a (batch, query head, 128-row query tile) like the
@@ -47,8 +48,8 @@ struct DkvParams {
   const float* rs;  // (lse2, delta) per query row
   bf16* dK;
   bf16* dV;
-  float* part;  // [2 (dK, dV)][clean-half key rows][D]: unscaled sums of the half of a clean key tile's walk that finished first
-  int* pair;    // per (clean key tile, key group): arrival count and ready flag, zeroed by the dq kernel
+  float* part;  // [nsplit - 1 arrival slots][2 (dK, dV)][clean-half key rows][D]: unscaled sums of the parts of a clean key tile's walk that did not finish last
+  int* pair;    // per (clean key tile, key group): DKV_PAIR_INTS counters (arrivals, published, slot owners), zeroed by the dq kernel
   SeqLayout seq;
   size_t seq_clean_rows;           // rows of one plane of `part`: clean-half keys of every sequence and KV head
   int L, S, Hq, Hkv, G, nKT, nkv;  // L: the (maximum) sequence length; nkv: sequences x KV heads
@@ -90,7 +91,7 @@ struct DkvSmem {
 // copies issued in a step stay in flight across it.  In step t the query-tile buffers
 // hold tiles t - 1 (consumer), t and t + 1 (producer), t + 2 (landed or
 // landing) and t + 3 (being copied); the P/dS buffers steps t and t - 1.
-template <int D>
+template <int D, int NSPLIT>
 __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   constexpr int BM = DKV_BM, BN = DKV_BN;
   constexpr int DS = D / 16, DB = D / 32;
@@ -102,8 +103,8 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int kg = w & 3;  // key group
   const int l32 = lane & 31, g2 = lane >> 5;
 
-  // Items: clean key tiles, most work first, each as two halves of its walk;
-  // then noisy key tiles, one item each.  Consecutive workgroups are
+  // Items: clean key tiles, most work first, each as nsplit parts of its
+  // walk; then noisy key tiles, one item each.  Consecutive workgroups are
   // different KV heads (or sequences).  A clean key tile at k0 is seen by
   // about 2 (L - k0) queries, so the work of a tile is set by how many tiles
   // of its sequence follow it: item rank r goes to the tile with nKT - r
@@ -113,15 +114,17 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int id = blockIdx.x;
   const int rank = id / p.nkv;
   const int grp = id - rank * p.nkv;  // b * Hkv + hk
-  const bool clean = rank < 2 * p.nKT;
+  constexpr int nsplit = NSPLIT;
+  const int crank = rank / nsplit;
+  const bool clean = rank < nsplit * p.nKT;
   const int kh = clean ? HALF_CLEAN : HALF_NOISY;
-  const int split = clean ? (rank & 1) : 0;
+  const int split = clean ? rank - crank * nsplit : 0;
   const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
   // sequence b: its length and where its rows lie
   int L;
   size_t qrow0, krow0, hrows;
   p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
-  const int j = clean ? (rank >> 1) - (p.nKT - cdiv(L, BN)) : rank - 2 * p.nKT;
+  const int j = clean ? crank - (p.nKT - cdiv(L, BN)) : rank - nsplit * p.nKT;
   if (j < 0 || j * BN >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
   // (a sequence shorter than S is one block: every formula below gives
   // the S = L mask then)
@@ -135,7 +138,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int kblock0 = kvalid ? (kk / S) * S : 0;
   const size_t krow = khead + kh * L + kk;
 
-  const QueryWalk wk = query_walk(kh, j, split, L, S, BM, BN, p.G);
+  const QueryWalk wk = query_walk(kh, j, split, nsplit, L, S, BM, BN, p.G);
   const int T = wk.steps();
   const int steps = T > 0 ? T + 1 : 0;  // the consumer trails the producer by one step
   const WalkPos first = wk.first(), last = wk.last();
@@ -325,30 +328,38 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     bf16* const outp = isdk ? p.dK : p.dV;
     const size_t orow = khead + kh * L;  // first row of this KV head's half
     if (clean) {
-      // The two halves of this key tile's walk meet here, per consumer wave:
-      // the first to arrive stores its float32 sums and raises the ready
-      // flag; the second waits for the flag (the first is running, since it
-      // has arrived), adds those sums to its own and writes its tensor.
-      // a + b == b + a in floating point, so the output does not depend on
-      // the order; the sums are stored unscaled and dK is scaled after the
-      // addition, so no multiply-add can fuse one side's product into the sum.
+      // The parts of this key tile's walk meet here, per consumer wave.  Each
+      // takes an arrival slot from the counter; every part but the last
+      // stores its float32 sums in its slot, records its part index for that
+      // slot (slots past the first; the part not found there is in slot 0)
+      // and then counts itself as published.  The last waits until every other
+      // part has published (each has arrived, so it is running and only
+      // stores), then adds the nsplit sums in part order, its own in place,
+      // and writes its tensor: the result is the same whichever part arrives
+      // when.  The sums are stored unscaled and dK is scaled after the
+      // addition, so no multiply-add can fuse one part's product into the sum.
       //
-      // The sums and the flag are written and read with device-scope (sc1)
-      // accesses, which the L2 of one XCD does not hold back from another,
-      // and the sums are complete (vmcnt) before the flag is stored.  Cache-wide
-      // release/acquire fences would instead write back and invalidate the
-      // whole L2 under the workgroups still running.
-      int* cnt = p.pair + 2 * ((j * p.nkv + grp) * 4 + c);
-      int* ready = cnt + 1;
+      // The sums, slot owners and counters are written and read with
+      // device-scope (sc1) accesses, which the L2 of one XCD does not hold
+      // back from another, and the sums and owner are complete (vmcnt) before
+      // the published count moves.  Cache-wide release/acquire fences would
+      // instead write back and invalidate the whole L2 under the workgroups
+      // still running.
+      int* cnt = p.pair + DKV_PAIR_INTS * ((j * p.nkv + grp) * 4 + c);
+      int* published = cnt + 1;
+      int* owner = cnt + 2;  // part index of the sums in each arrival slot
       // one row per clean-half key: this head's clean keys start at row khead / 2
       const size_t plane = (size_t)p.seq_clean_rows * D;
-      const float* pbase = p.part + (isdk ? 0 : plane) + (khead / 2) * D;
-      const __amdgpu_buffer_rsrc_t pr = make_buffer(pbase, (uint32_t)(L * D * 4));
+      auto slot_buffer = [&](int a) __attribute__((always_inline)) {
+        const float* pbase = p.part + (size_t)a * 2 * plane + (isdk ? 0 : plane) + (khead / 2) * D;
+        return make_buffer(pbase, (uint32_t)(L * D * 4));
+      };
       constexpr int SC1 = 16;  // cache-policy bit: device scope
       int order = 0;
       if (lane == 0) order = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       order = __builtin_amdgcn_readfirstlane(order);
-      if (order == 0) {
+      if (order < nsplit - 1) {
+        const __amdgpu_buffer_rsrc_t pr = slot_buffer(order);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           const int key = kc0 + 32 * ks + l32;
@@ -364,22 +375,25 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
               }
           }
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the sums have reached device scope
-        if (lane == 0) __hip_atomic_store(ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // (slot 0's owner is never read: a part missing from slots 1 .. is in slot 0)
+        if (order > 0 && lane == 0) __hip_atomic_store(owner + order, split, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the sums and the owner have reached device scope
+        if (lane == 0) __hip_atomic_fetch_add(published, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
       }
-      // Bounded wait (the first half is past its last step and only stores
+      // Bounded wait (every other part is past its last step and only stores
       // its sums); the bound only guarantees that the wave always ends.
       int seen = 0;
       for (int spin = 0; spin < (1 << 22); ++spin) {
-        seen = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        if (seen != 0) break;
+        seen = __builtin_amdgcn_readfirstlane(
+            __hip_atomic_load(published, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (seen == nsplit - 1) break;
         __builtin_amdgcn_s_sleep(2);
       }
       asm volatile("" ::: "memory");
-      if (seen == 0) {
-        // The other half's sums were never published: the result would be
-        // wrong, so this wave's keys get NaN instead of a plausible value.
+      if (seen != nsplit - 1) {
+        // Some part's sums were never published: the result would be wrong,
+        // so this wave's keys get NaN instead of a plausible value.
         const float nan = __builtin_nanf("");
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
@@ -394,6 +408,19 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
         }
         return;
       }
+      // the part whose sums arrival slots 1 and 2 hold (-1: no such slot; two
+      // parts have none)
+      int own_of[3] = {-1, -1, -1};
+#pragma unroll
+      for (int a = 1; a < nsplit - 1; ++a)
+        own_of[a] = __builtin_amdgcn_readfirstlane(
+            __hip_atomic_load(owner + a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      // arrival slot of part q: slot 0 unless slot 1 or 2 holds it (also for
+      // this part, whose sums are its own: a valid slot, so that a load the
+      // compiler issues anyway stays in bounds)
+      auto slot_of = [&](int q) __attribute__((always_inline)) {
+        return q == own_of[1] ? 1 : q == own_of[2] ? 2 : 0;
+      };
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const int key = kc0 + 32 * ks + l32;
@@ -404,9 +431,17 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
           for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const f32x4 o = __builtin_amdgcn_raw_buffer_load_b128(pr, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-              st_bf16x4(op + db * 32 + 8 * i, (acc[ks][db][4 * i] + o[0]) * sc, (acc[ks][db][4 * i + 1] + o[1]) * sc,
-                        (acc[ks][db][4 * i + 2] + o[2]) * sc, (acc[ks][db][4 * i + 3] + o[3]) * sc);
+              const f32x4 own = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
+                                 acc[ks][db][4 * i + 3]};
+              f32x4 tot = own;
+#pragma unroll
+              for (int q = 0; q < nsplit; ++q) {
+                const f32x4 x = q == split ? own
+                                           : __builtin_amdgcn_raw_buffer_load_b128(
+                                                 slot_buffer(slot_of(q)), poff + 4 * (db * 32 + 8 * i), 0, SC1);
+                tot = q == 0 ? x : tot + x;
+              }
+              st_bf16x4(op + db * 32 + 8 * i, tot[0] * sc, tot[1] * sc, tot[2] * sc, tot[3] * sc);
             }
         }
       }
@@ -700,8 +735,12 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.nkv = s.B * s.Hkv;
   p.c = s.scale * LOG2E;
   p.scale = s.scale;
-  const dim3 grid(3 * p.nKT * p.nkv);
-  hipLaunchKernelGGL(dkdv_kernel<D>, grid, dim3(512), 0, st, p);
+  // each clean key tile's walk in 2 or 4 parts, then the noisy key tiles
+  if (dkdv_nsplit(s) == 4) {
+    hipLaunchKernelGGL((dkdv_kernel<D, 4>), dim3(5 * p.nKT * p.nkv), dim3(512), 0, st, p);
+  } else {
+    hipLaunchKernelGGL((dkdv_kernel<D, 2>), dim3(3 * p.nKT * p.nkv), dim3(512), 0, st, p);
+  }
   return hipGetLastError();
 }
 

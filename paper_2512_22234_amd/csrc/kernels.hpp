@@ -60,9 +60,9 @@ hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* 
 //   dq:   dQ, and per query row the float32 pair (lse2, delta) =
 //         (LSE * log2(e), rowsum(dO * O)) interleaved in rs[2 * row], rs[2 * row + 1]
 //         (B*Hq*2L rows); also zeroes the dK/dV pairing counters `pair`.
-//   dkdv: dK and dV.  Each clean key tile's walk runs as two halves; the half
-//         that finishes first leaves float32 sums in `part` (dkdv_partial_floats
-//         elements), the other adds them to its own.
+//   dkdv: dK and dV.  Each clean key tile's walk runs in dkdv_nsplit(s) parts;
+//         every part but the last to finish leaves float32 sums in `part`
+//         (dkdv_partial_floats elements), the last adds them to its own.
 hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
                          const void* O, const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st);
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V,
@@ -75,13 +75,34 @@ hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const v
 inline size_t dkdv_clean_rows(const Shape& s) {
   return s.seq.cu ? (size_t)s.Hkv * s.seq.T : (size_t)s.B * s.Hkv * s.L;
 }
-// float32 sums of one half of the clean key tiles' walks: dK and dV, one row
-// per clean-half key.
-inline size_t dkdv_partial_floats(const Shape& s) { return 2 * dkdv_clean_rows(s) * s.D; }
-// Pairing counters: per (clean key tile, batch x KV head, key group of 32) an
-// arrival count and a ready flag.
+// Parts each clean key tile's dK/dV walk is split into: 2, or 4 when half of
+// the heaviest walk would be much longer than the average work of one CU, so
+// that the kernel would end with its longest items.  Half of key tile 0's
+// walk takes about G L / 32 steps; all clean walks of one sequence and KV head
+// take about G L (L + 128) / 4096, so over the 256 CUs of the part the ratio is
+// 32768 / (nkv (L + 128)), nkv being the sequences times KV heads (for packed
+// sequences, the tokens per copy over the longest length).  Results stay
+// bitwise reproducible for a given shape: the parts' sums are added in part
+// order, whichever finishes first.
+constexpr int DKV_CUS = 256;
+inline int dkdv_nsplit(int B, int Hkv, int L, const SeqLayout& seq) {
+  const double nkv = seq.cu ? (double)Hkv * seq.T / L : (double)B * Hkv;
+  const double ratio = (double)DKV_CUS * 128 / (nkv * (L + 128));
+  return ratio >= 1.5 ? 4 : 2;
+}
+inline int dkdv_nsplit(const Shape& s) { return dkdv_nsplit(s.B, s.Hkv, s.L, s.seq); }
+// float32 sums of the parts of the clean key tiles' walks that do not finish
+// last: per arrival slot (nsplit - 1 of them) dK and dV, one row per
+// clean-half key.
+inline size_t dkdv_partial_floats(const Shape& s) {
+  return (size_t)(dkdv_nsplit(s) - 1) * 2 * dkdv_clean_rows(s) * s.D;
+}
+// Pairing counters: per (clean key tile, batch x KV head, key group of 32)
+// eight ints: the arrival count, the count of parts that have published their
+// sums, and for each arrival slot the part index whose sums it holds.
+constexpr int DKV_PAIR_INTS = 8;
 inline size_t dkdv_pair_ints(int B, int Hkv, int L) {
-  return (size_t)2 * 4 * B * Hkv * ((L + DKV_BN - 1) / DKV_BN);
+  return (size_t)DKV_PAIR_INTS * 4 * B * Hkv * ((L + DKV_BN - 1) / DKV_BN);
 }
 
 // Block decoding over a KV cache: B sequences, each decoding a block of S

@@ -298,22 +298,23 @@ BD_HD WalkPos QueryWalk::last() const {
 
 // Walk of key tile (kh, j).  A clean key tile is seen by noisy query tiles
 // [noisy0, nQT) and clean ones [clean0, nQT), clean0 <= noisy0; it is done by
-// two workgroups (split 0 and 1) whose walks take alternate tiles from the
-// top down, so they have equal work to within one tile.  A noisy key tile is
-// seen by noisy query tiles [noisy0, noisy0 + nnoisy) only and is done by one
-// workgroup (split 0).  Walks start at the highest tile and move down, heads
-// innermost, so the workgroups of all key tiles of one KV group read the same
-// query tile at about the same time.
-BD_HD QueryWalk query_walk(int kh, int j, int split, int L, int S, int BM, int BN, int G) {
+// nsplit workgroups (split 0 .. nsplit - 1) whose walks take every nsplit-th
+// tile from the top down, starting at tile nQT - 1 - split, so they have
+// equal work to within one tile.  A noisy key tile is seen by noisy query
+// tiles [noisy0, noisy0 + nnoisy) only and is done by one workgroup (split
+// 0).  Walks start at the highest tile and move down, heads innermost, so the
+// workgroups of all key tiles of one KV group read the same query tile at
+// about the same time.
+BD_HD QueryWalk query_walk(int kh, int j, int split, int nsplit, int L, int S, int BM, int BN, int G) {
   const QueryTileList ql = query_tiles_for_key_tile(kh, j, L, S, BM, BN);
   QueryWalk wk;
   wk.G = G;
   if (kh == HALF_CLEAN) {
     const int nQT = ql.clean0 + ql.nclean;
     wk.u0 = nQT - 1 - split;
-    wk.du = -2;
-    wk.K = wk.u0 >= ql.clean0 ? (wk.u0 - ql.clean0) / 2 + 1 : 0;
-    wk.K2 = (ql.nnoisy > 0 && wk.u0 >= ql.noisy0) ? imin(wk.K, (wk.u0 - ql.noisy0) / 2 + 1) : 0;
+    wk.du = -nsplit;
+    wk.K = wk.u0 >= ql.clean0 ? (wk.u0 - ql.clean0) / nsplit + 1 : 0;
+    wk.K2 = (ql.nnoisy > 0 && wk.u0 >= ql.noisy0) ? imin(wk.K, (wk.u0 - ql.noisy0) / nsplit + 1) : 0;
     wk.rest = HALF_CLEAN;
   } else {
     wk.u0 = ql.noisy0 + ql.nnoisy - 1;

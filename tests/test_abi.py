@@ -78,9 +78,17 @@ def test_classifier_matches_explicit_mask(L, S, BM, BN):
                                                     (33, 40, 32, 128), (1, 1, 32, 128)])
 def test_tile_walks_visit_each_nonempty_pair_once(L, S, BM, BN):
     cls = bd.bd_attn_classify_tiles_host(L, S, BM, BN)
-    for by_key in (False, True):
-        visits = bd.bd_attn_visit_lists_host(L, S, BM, BN, by_key)
-        np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"by_key={by_key}")
+    visits = bd.bd_attn_visit_lists_host(L, S, BM, BN, False)
+    np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg="by query tile")
+    # the dK/dV walks, with each clean key tile's walk in 2 or 4 parts
+    for nsplit in (2, 4):
+        visits = bd.bd_attn_visit_lists_host(L, S, BM, BN, True, nsplit)
+        np.testing.assert_array_equal(visits, (cls != 0).astype(np.int8), err_msg=f"by key tile, {nsplit} parts")
+
+
+def test_walk_split_count_is_validated():
+    with pytest.raises(bd.BdAttnError):
+        bd.bd_attn_visit_lists_host(64, 4, 32, 128, True, 3)
 
 
 def test_forward_full_prefix_holds_only_full_tiles():
@@ -142,6 +150,24 @@ def test_workspace_bytes():
     assert f(2, 2048, 4, 32, 8, 96, 0, 0) == 0       # D unsupported
     assert f(2, 0, 4, 32, 8, 128, 0, 0) == 0         # L < 1
     assert f(2, 2048, 4, 32, 8, 128, 7, 0) == 0      # dtype
+
+
+def test_workspace_bytes_follow_the_dkdv_split():
+    """bf16 backward workspace = (lse2, delta) per query row + float32 sums of
+    nsplit - 1 parts of the clean key tiles' walks (dK and dV, one row per
+    clean-half key) + 32 pairing ints per (clean key tile, sequence x KV head)
+    (each piece rounded up to 256 bytes).  Few KV heads x length (the small
+    configuration) split each walk in four parts, the 8B one in two."""
+    f = bd.bd_attn_workspace_bytes
+
+    def want(B, L, Hq, Hkv, D, nsplit):
+        r256 = lambda x: -(-x // 256) * 256
+        return (r256(B * Hq * 2 * L * 8) + r256((nsplit - 1) * 2 * B * Hkv * L * D * 4)
+                + r256(32 * B * Hkv * (-(-L // 128)) * 4))
+
+    assert f(4, 1024, 4, 16, 4, 64, 0, 1) == want(4, 1024, 16, 4, 64, 4) == 26_230_784
+    assert f(2, 2048, 4, 32, 8, 128, 0, 1) == want(2, 2048, 32, 8, 128, 2) == 35_684_352
+    assert f(1, 8192, 4, 32, 8, 128, 0, 1) == want(1, 8192, 32, 8, 128, 2)
 
 
 # Fake, never-dereferenced device addresses: every call below fails validation
