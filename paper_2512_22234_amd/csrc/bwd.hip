@@ -72,8 +72,18 @@ struct DkvSmem {
   static constexpr uint32_t XBUF = 4 * XGRP;
   static_assert(BUF % 256 == 0 && XBUF % 256 == 0, "operand addressing needs 256-byte aligned tiles");
   static_assert(BM == 32, "one 32-query block per step");
-  alignas(256) char buf[NBUF][BUF];
-  alignas(256) char x[2][XBUF];
+  // Noisy key tiles whose key groups each see one 32-query block (S divides
+  // 32): two sets of the four query tiles under the key tile (one query head
+  // each) and one P/dS buffer.
+  static constexpr int NBUF_NOISY = 8;
+  static constexpr uint32_t CLEAN_BYTES = NBUF * BUF + 2 * XBUF, NOISY_BYTES = NBUF_NOISY * BUF + XBUF;
+  alignas(256) char mem[CLEAN_BYTES > NOISY_BYTES ? CLEAN_BYTES : NOISY_BYTES];
+  // clean key tiles: query-tile buffer i, P/dS buffer i
+  __device__ char* buf(int i) { return mem + i * BUF; }
+  __device__ char* x(int i) { return mem + NBUF * BUF + i * XBUF; }
+  // noisy key tiles: query tile u (of four) of set `set`, and the P/dS buffer
+  __device__ char* nbuf(int set, int u) { return mem + (4 * set + u) * BUF; }
+  __device__ char* nx() { return mem + NBUF_NOISY * BUF; }
 };
 
 // Workgroup of eight waves on one (batch, KV head, 128-key tile).  Waves w and
@@ -138,6 +148,12 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int kblock0 = kvalid ? (kk / S) * S : 0;
   const size_t krow = khead + kh * L + kk;
 
+  // A noisy key group is seen only by the noisy queries of its own blocks;
+  // when S divides 32 those are exactly the 32 queries at the same positions,
+  // so each producer scores its own query block and a noisy key tile takes one
+  // step per query head (a walk over the four query tiles would leave three
+  // of the four producers without a visible pair in every step).
+  const bool noisy_diag = !clean && 32 % S == 0;
   const QueryWalk wk = query_walk(kh, j, split, nsplit, L, S, BM, BN, p.G);
   const int T = wk.steps();
   const int steps = T > 0 ? T + 1 : 0;  // the consumer trails the producer by one step
@@ -207,10 +223,10 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       const int qh = cur.qh, q0 = cur.tile(wk) * BM;
       cur.next(wk);
       const uint32_t bnext = bcur == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcur + Smem::BUF;
-      const char* bt = sm.buf[0] + bcur;
-      const char* bn = sm.buf[0] + bnext;
+      const char* bt = sm.mem + bcur;
+      const char* bn = sm.mem + bnext;
       bcur = bnext;
-      char* xw = sm.x[t & 1];
+      char* xw = sm.x(t & 1);
       // (EMPTY tiles are never visited; the window test would mask all of one)
       if (fr.full(qh, q0, BM)) {
         scores(bn, sn, dn);
@@ -221,9 +237,25 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
         softmax_grad(bt, xw, sc, dc, q0 + 4 * g2 - win.lo, (unsigned)(win.hi - win.lo), Flag<true>());
       }
     };
+    if (noisy_diag) {
+      // Per query head g: S and dP of this key group against query block kg
+      // of set g % 2, then P and dS (visibility window per element), written
+      // for the consumers; no software pipeline (one step per head).
+      const unsigned span = (unsigned)(win_n.hi - win_n.lo);
+      const int rel = k0 + 32 * kg + 4 * g2 - win_n.lo;
+      for (int g = 0; g < p.G; ++g) {
+        barrier_lds_only();  // set g % 2 has landed; the consumers are done with the P/dS buffer
+        const char* bt = sm.nbuf(g & 1, kg);
+        f32x16 sc, dc;
+        scores(bt, sc, dc);
+        softmax_grad(bt, sm.nx(), sc, dc, rel, span, Flag<true>());
+        barrier_lds_only();  // P and dS are written
+      }
+      return;
+    }
     f32x16 sA, dA, sB, dB;
     __syncthreads();  // the first three query tiles are in LDS
-    if (T > 0) scores(sm.buf[0], sA, dA);
+    if (T > 0) scores(sm.mem, sA, dA);
     // steps alternate the two accumulator pairs (unrolled by two, no copies)
     for (int t = 0; t < T; t += 2) {
       step(t, sA, dA, sB, dB);
@@ -260,15 +292,6 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       copy.issue_rows(dog + r * D, left, dst + Smem::DO_OFF);
       async_load_row_floats(rsg + 2 * r, 2 * left, 0, reinterpret_cast<float*>(dst + Smem::RS_OFF), lane);
     };
-    // tiles 0, 1 and 2 (the last tile again past the end); cp then points at tile 3
-    WalkPos cp = first;
-    if (T > 0) {
-#pragma unroll
-      for (int u = 0; u < 3; ++u) {
-        issue(u < T ? cp : last, sm.buf[u]);
-        cp.next(wk);
-      }
-    }
     f32x16 acc[2][DB];  // [key group of 32][feature block of 32]
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
@@ -276,6 +299,61 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[ks][db][e] = 0.f;
+    const uint32_t aoff = isdk ? 0u : Smem::DO_OFF;  // A operand: Q^T or dO^T
+    const int xsel = isdk ? 1 : 0;                   // B operand: dS or P
+    if (noisy_diag) {
+      // The four noisy query tiles under the key tile, for query head g,
+      // into set s (two sets: head g + 1 lands while head g is computed).
+      auto issue_head = [&](int g, int set) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int row0 = k0 + 32 * u;  // noisy half: local position = row
+          const size_t r = (size_t)g * hrows + row0;
+          const int left = N - row0;
+          char* dst = sm.nbuf(set, u);
+          copy.issue_rows(qg + r * D, left, dst);
+          copy.issue_rows(dog + r * D, left, dst + Smem::DO_OFF);
+          async_load_row_floats(rsg + 2 * r, 2 * left, 0, reinterpret_cast<float*>(dst + Smem::RS_OFF), lane);
+        }
+      };
+      issue_head(0, 0);
+      if (p.G > 1) issue_head(1, 1);
+      for (int g = 0; g < p.G; ++g) {
+        // set g % 2 has landed in this wave's part (before head 0 the copy of
+        // head 1 may still be in flight; later the copy in flight is head g's,
+        // issued in the previous iteration) ...
+        if (g == 0 && p.G > 1) wait_global_loads_but<4 * NC>();
+        else wait_global_loads();
+        barrier_lds_only();  // ... and in every wave's
+        // set (g + 1) % 2 held head g - 1, which everyone is done with
+        if (g >= 1 && g + 1 < p.G) issue_head(g + 1, (g + 1) & 1);
+        barrier_lds_only();  // the producers have written P and dS of head g
+        // key group 2 (c % 2) + ks saw query block 2 (c % 2) + ks of the set
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int grp4 = 2 * (c & 1) + ks;
+          const char* bc = sm.nbuf(g & 1, grp4);
+          bf16x8 xb[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            xb[h] = *reinterpret_cast<const bf16x8*>(sm.nx() + grp4 * Smem::XGRP + 16 * lane + (2 * h + xsel) * 1024);
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+              acc[ks][db] = mfma32(lds_tr<D>(bc + aoff, ops.tr_rel0, ops.tr_rel1, h, db), xb[h], acc[ks][db]);
+        }
+      }
+    } else {
+    // tiles 0, 1 and 2 (the last tile again past the end); cp then points at tile 3
+    WalkPos cp = first;
+    if (T > 0) {
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        issue(u < T ? cp : last, sm.buf(u));
+        cp.next(wk);
+      }
+    }
     wait_global_loads();
     __syncthreads();
 
@@ -286,8 +364,6 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // compiler does not wait for the copy in flight before the reads.
     //   dV^T[d][key] += sum_q dO^T[d][q] P[q][key]   (dV consumers)
     //   dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]   (dK consumers)
-    const uint32_t aoff = isdk ? 0u : Smem::DO_OFF;  // A operand: Q^T or dO^T
-    const int xsel = isdk ? 1 : 0;                   // B operand: dS or P
     auto consume = [&](const char* __restrict__ bc, const char* __restrict__ xr, char* __restrict__ bn, int t)
                        __attribute__((always_inline)) {
       if (t > 0) {
@@ -314,13 +390,14 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     uint32_t bcons = (Smem::NBUF - 1) * Smem::BUF;  // buffer of tile t - 1
     uint32_t bcopy = 3 * Smem::BUF;                  // buffer tile t + 3 is copied into
     for (int t = 0; t < steps; ++t) {
-      consume(sm.buf[0] + bcons, sm.x[(t + 1) & 1], sm.buf[0] + bcopy, t);
+      consume(sm.mem + bcons, sm.x((t + 1) & 1), sm.mem + bcopy, t);
       bcons = bcons == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcons + Smem::BUF;
       bcopy = bcopy == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcopy + Smem::BUF;
       if (t + 3 < T) cp.next(wk);
       compute_fence();
       wait_global_loads_but<NC>();  // tile t + 2 has landed (the copy issued this step may not have)
       barrier_lds_only();           // ... in every wave's part; the copy in flight stays in flight
+    }
     }
     wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 
