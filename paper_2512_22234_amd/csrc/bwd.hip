@@ -114,28 +114,54 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   const int l32 = lane & 31, g2 = lane >> 5;
 
   // Items: clean key tiles, most work first, each as nsplit parts of its
-  // walk; then noisy key tiles, one item each.  Consecutive workgroups are
-  // different KV heads (or sequences).  A clean key tile at k0 is seen by
-  // about 2 (L - k0) queries, so the work of a tile is set by how many tiles
-  // of its sequence follow it: item rank r goes to the tile with nKT - r
-  // tiles from it to its sequence's end (nKT: the tile count of the longest
-  // sequence), which is tile r itself when every sequence has the maximum
-  // length.
+  // walk; then noisy key tiles, one item each.  A clean key tile at k0 is seen
+  // by about 2 (L - k0) queries, so the work of a tile is set by how many
+  // tiles of its sequence follow it.  Fixed length: item rank r is tile r,
+  // consecutive workgroups being different KV heads and sequences.  Packed
+  // sequences: one ranking of all sequences' key tiles by the tiles from each
+  // to its sequence's end, largest first (the grid is sized by a bound on
+  // their count); the parts and KV heads of one tile are consecutive items.
   const int id = blockIdx.x;
-  const int rank = id / p.nkv;
-  const int grp = id - rank * p.nkv;  // b * Hkv + hk
   constexpr int nsplit = NSPLIT;
-  const int crank = rank / nsplit;
-  const bool clean = rank < nsplit * p.nKT;
+  int b, hk, split, j;
+  bool clean;
+  int pc0 = 0, plen = 0;  // packed: the sequence's first token and length
+  if (p.seq.cu == nullptr) {
+    const int rank = id / p.nkv;
+    const int grp0 = id - rank * p.nkv;  // b * Hkv + hk
+    const int crank = rank / nsplit;
+    clean = rank < nsplit * p.nKT;
+    split = clean ? rank - crank * nsplit : 0;
+    b = grp0 / p.Hkv;
+    hk = grp0 - b * p.Hkv;
+    j = clean ? crank : rank - nsplit * p.nKT;
+  } else {
+    const int n = p.nkv / p.Hkv;
+    const int nclean = nsplit * p.Hkv * packed_rows(p.seq.cu, n, BN);
+    int r;
+    clean = id < nclean;
+    if (clean) {
+      r = id / (nsplit * p.Hkv);
+      const int q = id - r * nsplit * p.Hkv;
+      split = q / p.Hkv;
+      hk = q - split * p.Hkv;
+    } else {
+      r = (id - nclean) / p.Hkv;
+      hk = id - nclean - r * p.Hkv;
+      split = 0;
+    }
+    int i, nt;
+    if (!packed_row(p.seq.cu, n, p.nKT, BN, r, b, i, nt, pc0, plen)) return;  // past the last tile
+    j = nt - 1 - i;
+  }
   const int kh = clean ? HALF_CLEAN : HALF_NOISY;
-  const int split = clean ? rank - crank * nsplit : 0;
-  const int b = grp / p.Hkv, hk = grp - b * p.Hkv;
+  const int grp = b * p.Hkv + hk;
   // sequence b: its length and where its rows lie
   int L;
   size_t qrow0, krow0, hrows;
-  p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
-  const int j = clean ? crank - (p.nKT - cdiv(L, BN)) : rank - nsplit * p.nKT;
-  if (j < 0 || j * BN >= L) return;  // a shorter sequence than the grid is sized for (whole workgroup)
+  if (p.seq.cu == nullptr) p.seq.get(b, p.L, p.Hq, p.Hkv, L, qrow0, krow0, hrows);
+  else p.seq.get_packed(pc0, plen, L, qrow0, krow0, hrows);
+  if (j * BN >= L) return;  // (fixed length: never)
   // (a sequence shorter than S is one block: every formula below gives
   // the S = L mask then)
   const int S = p.S;
@@ -813,10 +839,12 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.c = s.scale * LOG2E;
   p.scale = s.scale;
   // each clean key tile's walk in 2 or 4 parts, then the noisy key tiles
+  // (packed sequences: grid sized by a bound on the key tiles of all sequences)
+  const int rows = s.seq.cu ? packed_rows_bound(s.seq.T, s.B, s.L, DKV_BN) : p.nKT * s.B;
   if (dkdv_nsplit(s) == 4) {
-    hipLaunchKernelGGL((dkdv_kernel<D, 4>), dim3(5 * p.nKT * p.nkv), dim3(512), 0, st, p);
+    hipLaunchKernelGGL((dkdv_kernel<D, 4>), dim3(5 * rows * s.Hkv), dim3(512), 0, st, p);
   } else {
-    hipLaunchKernelGGL((dkdv_kernel<D, 2>), dim3(3 * p.nKT * p.nkv), dim3(512), 0, st, p);
+    hipLaunchKernelGGL((dkdv_kernel<D, 2>), dim3(3 * rows * s.Hkv), dim3(512), 0, st, p);
   }
   return hipGetLastError();
 }

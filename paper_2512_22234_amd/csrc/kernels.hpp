@@ -34,7 +34,73 @@ struct SeqLayout {
       qrow = krow = 2 * (size_t)c0;
     }
   }
+  // The same for a packed sequence whose first token and length are known.
+  __device__ void get_packed(int c0, int len, int& Ls, size_t& qrow, size_t& krow, size_t& hrows) const {
+    Ls = len;
+    hrows = 2 * (size_t)T;
+    qrow = krow = 2 * (size_t)c0;
+  }
 };
+
+// Packed sequences: the tiles of all sequences ranked heaviest first.  Each
+// sequence s of length len_s has nt_s = cdiv(len_s, tile) tiles per half;
+// row r of the ranking is the pair (s, i) in the order i = ntmax - 1 down to
+// 0 and, for one i, the sequences with nt_s > i in order.  (The dK/dV kernel
+// ranks its key tiles this way: the work of a key tile grows with the tiles
+// after it, so row (s, i) stands for key tile nt_s - 1 - i.)  Every lane of
+// the wave calls this with the same r and receives the same result; false
+// when r is past the last row.  One ballot per (i, 64 sequences).  Also returns the
+// sequence's first token c0 and length len (as SeqLayout::get would read them).
+__device__ inline bool packed_row(const int* __restrict__ cu, int n, int ntmax, int tile, int r, int& s_out,
+                                  int& i_out, int& nt_out, int& c0_out, int& len_out) {
+  const int lane = threadIdx.x & 63;
+  int rem = r;
+  // up to 64 sequences (one per lane): their bounds are loaded once
+  const int lo0 = lane < n ? cu[lane] : 0, hi0 = lane < n ? cu[lane + 1] : 0;
+  for (int i = ntmax - 1; i >= 0; --i) {
+    for (int base = 0; base < n; base += 64) {
+      const int s = base + lane;
+      const int lo = base == 0 ? lo0 : s < n ? cu[s] : 0;
+      const int hi = base == 0 ? hi0 : s < n ? cu[s + 1] : 0;
+      const int nt = (hi - lo + tile - 1) / tile;
+      const unsigned long long m = __ballot(nt > i);
+      const int cnt = __popcll(m);
+      if (rem < cnt) {
+        // the rem-th sequence of this chunk with more than i tiles
+        const int below = __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        const unsigned long long sel = __ballot(nt > i && below == rem);
+        const int l = __ffsll((long long)sel) - 1;
+        s_out = __builtin_amdgcn_readfirstlane(base + l);
+        i_out = i;
+        nt_out = __builtin_amdgcn_readfirstlane(__shfl(nt, l));
+        c0_out = __builtin_amdgcn_readfirstlane(__shfl(lo, l));
+        len_out = __builtin_amdgcn_readfirstlane(__shfl(hi - lo, l));
+        return true;
+      }
+      rem -= cnt;
+    }
+  }
+  return false;
+}
+// Rows of that ranking: the tiles per half of all sequences.  Same calling
+// convention.
+__device__ inline int packed_rows(const int* __restrict__ cu, int n, int tile) {
+  const int lane = threadIdx.x & 63;
+  int sum = 0;
+  for (int base = 0; base < n; base += 64) {
+    const int s = base + lane;
+    sum += s < n ? (cu[s + 1] - cu[s] + tile - 1) / tile : 0;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+  return __builtin_amdgcn_readfirstlane(sum);
+}
+// Host bound on those rows: sum over s of cdiv(len_s, tile) <= T / tile + n,
+// and at most n cdiv(max_L, tile).
+inline int packed_rows_bound(int T, int n, int max_L, int tile) {
+  const long long a = (long long)T / tile + n, b = (long long)n * ((max_L + tile - 1) / tile);
+  return (int)(a < b ? a : b);
+}
 
 struct Shape {
   int B, L, S, Hq, Hkv, D;  // B sequences of length L (packed: B sequences, L bounds their lengths)
