@@ -48,6 +48,32 @@ struct FwdSmem {
 // reference).
 constexpr float RESCALE_SLACK = 8.0f;
 
+// Maximum of N values as a balanced tree (depth log2 N instead of a chain of N).
+template <int N>
+__device__ inline float tree_max(const float* v) {
+  if constexpr (N == 1) {
+    return v[0];
+  } else {
+    return fmaxf(tree_max<N / 2>(v), tree_max<N - N / 2>(v + N / 2));
+  }
+}
+// Sum of the 16 K entries of K accumulators as a balanced tree.
+template <int K>
+__device__ inline float tree_sum(const f32x16* a) {
+  float t[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    t[e] = a[0][e];
+#pragma unroll
+    for (int k = 1; k < K; ++k) t[e] += a[k][e];
+  }
+#pragma unroll
+  for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+    for (int e = 0; e < w; ++e) t[e] += t[e + w];
+  return t[0];
+}
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
   constexpr int BM = FWD_BM, BN = FWD_BN;
@@ -177,11 +203,13 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
       // K operand reads four MFMAs ahead, the copies spread between the MFMAs
       pipeline_reads_and_copies<DS * KB, 4, 1, 2 * decltype(copy)::NI>();
       // (a FULL tile: every key is visible from every row, no test)
-      float mx = -INFINITY;
+      // row maximum as a tree of three-input maxima (no serial chain)
+      float m3[KB * 16 / 2];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[kb][e], sacc[kb][e + 1]));
+        for (int e = 0; e < 16; e += 2) m3[kb * 8 + e / 2] = fmaxf(sacc[kb][e], sacc[kb][e + 1]);
+      float mx = tree_max<KB * 8>(m3);
       mx = halves_max(mx) * p.c;
       // move the reference only when this tile's max is far above it
       const bool grow = mx > m + RESCALE_SLACK;
@@ -202,11 +230,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float x = fast_exp2(sacc[kb][e] * p.c - muse);
-          sacc[kb][e] = x;
-          lsum += x;
-        }
+        for (int e = 0; e < 16; ++e) sacc[kb][e] = fast_exp2(sacc[kb][e] * p.c - muse);
+      // the tile's row sum as a tree (no serial chain of 32 additions)
+      lsum += tree_sum<KB>(sacc);
       bf16x8 pb[PC];
 #pragma unroll
       for (int c = 0; c < PC; ++c) pb[c] = pack8(sacc[c >> 1], 8 * (c & 1));
@@ -239,9 +265,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
         const unsigned pos = (unsigned)(rel + 8 * i + jj);
         sa[4 * i + jj] = pos < span ? sa[4 * i + jj] : -INFINITY;
       }
-    float mx = -INFINITY;
+    float m3[8];
 #pragma unroll
-    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sa[e], sa[e + 1]));
+    for (int e = 0; e < 16; e += 2) m3[e / 2] = fmaxf(sa[e], sa[e + 1]);
+    float mx = tree_max<8>(m3);
     mx = halves_max(mx) * p.c;
     const bool grow = mx > m + RESCALE_SLACK;
     if (__any(grow)) {
@@ -257,11 +284,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
     }
     const float muse = (m == -INFINITY) ? 0.f : m;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float x = fast_exp2(sa[e] * p.c - muse);
-      sa[e] = x;
-      lsum += x;
-    }
+    for (int e = 0; e < 16; ++e) sa[e] = fast_exp2(sa[e] * p.c - muse);
+    lsum += tree_sum<1>(&sa);
     const bf16x8 p0 = pack8(sa, 0), p1 = pack8(sa, 8);
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = mfma32(lds_tr<D>(vcur, ops.tr_rel0, ops.tr_rel1, 2 * kb, db), p0, oacc[db]);
