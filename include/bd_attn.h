@@ -113,7 +113,8 @@ int bd_attn_bwd(const void* dO, const void* Q, const void* K, const void* V,
  * library's first use on that GPU until the process ends.  A problem whose
  * bd_attn_workspace_bytes(..., for_bwd = 1) exceeds it is rejected with
  * BD_ATTN_ERR_EXCEEDS_SCRATCH before anything is enqueued (in bfloat16 the
- * workspace is B*Hq*2L*8 + (n-1)*B*Hkv*L*D*8 bytes plus a few KiB, where n is
+ * workspace is B*Hq*2L*8 + (n-1)*B*Hkv*L'*D*8 bytes plus a few KiB (L' = L rounded
+ * up to a multiple of 128), where n is
  * the number of parts each clean key tile's dK/dV walk is split into: 4 when
  * B*Hkv*(L+128) <= 21845, else 2; 34.0 MiB for B=2, Hq=32, Hkv=8, D=128,
  * L=2048 and 68.0 MiB for B=1, L=8192 at the same heads; float32 inputs also

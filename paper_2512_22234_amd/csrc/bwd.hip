@@ -48,10 +48,10 @@ struct DkvParams {
   const float* rs;  // (lse2, delta) per query row
   bf16* dK;
   bf16* dV;
-  float* part;  // [nsplit - 1 arrival slots][2 (dK, dV)][clean-half key rows][D]: unscaled sums of the parts of a clean key tile's walk that did not finish last
+  float* part;  // [nsplit - 1 arrival slots][tile slots][4 consumer waves][32 x 16 bytes per lane]: unscaled sums of the parts of a clean key tile's walk that did not finish last
   int* pair;    // per (clean key tile, key group): DKV_PAIR_INTS counters (arrivals, published, slot owners), zeroed by the dq kernel
   SeqLayout seq;
-  size_t seq_clean_rows;           // rows of one plane of `part`: clean-half keys of every sequence and KV head
+  size_t tile_slots;               // regions of one arrival slot of `part`: clean key tiles of every sequence and KV head
   int L, S, Hq, Hkv, G, nKT, nkv;  // L: the (maximum) sequence length; nkv: sequences x KV heads
   float c;      // scale * log2(e)
   float scale;
@@ -126,6 +126,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
   int b, hk, split, j;
   bool clean;
   int pc0 = 0, plen = 0;  // packed: the sequence's first token and length
+  size_t tslot;           // region of the partial sums of this key tile (clean items)
   if (p.seq.cu == nullptr) {
     const int rank = id / p.nkv;
     const int grp0 = id - rank * p.nkv;  // b * Hkv + hk
@@ -135,6 +136,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     b = grp0 / p.Hkv;
     hk = grp0 - b * p.Hkv;
     j = clean ? crank : rank - nsplit * p.nKT;
+    tslot = (size_t)j * p.nkv + grp0;
   } else {
     const int n = p.nkv / p.Hkv;
     const int nclean = nsplit * p.Hkv * packed_rows(p.seq.cu, n, BN);
@@ -153,6 +155,7 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     int i, nt;
     if (!packed_row(p.seq.cu, n, p.nKT, BN, r, b, i, nt, pc0, plen)) return;  // past the last tile
     j = nt - 1 - i;
+    tslot = (size_t)r * p.Hkv + hk;
   }
   const int kh = clean ? HALF_CLEAN : HALF_NOISY;
   const int grp = b * p.Hkv + hk;
@@ -448,15 +451,20 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       // the published count moves.  Cache-wide release/acquire fences would
       // instead write back and invalidate the whole L2 under the workgroups
       // still running.
+      //
+      // The sums travel in the register order of the consumer waves (the
+      // same in every part): accumulator quad u = (ks DB + db) 4 + i of lane
+      // l at byte 1024 u + 16 l of this wave's 32 KiB region, so each store
+      // or load instruction moves 1 KiB of consecutive bytes (a layout by key
+      // row would write 32-byte pieces of 32 rows per instruction).
       int* cnt = p.pair + DKV_PAIR_INTS * ((j * p.nkv + grp) * 4 + c);
       int* published = cnt + 1;
       int* owner = cnt + 2;  // part index of the sums in each arrival slot
-      // one row per clean-half key: this head's clean keys start at row khead / 2
-      const size_t plane = (size_t)p.seq_clean_rows * D;
       auto slot_buffer = [&](int a) __attribute__((always_inline)) {
-        const float* pbase = p.part + (size_t)a * 2 * plane + (isdk ? 0 : plane) + (khead / 2) * D;
-        return make_buffer(pbase, (uint32_t)(L * D * 4));
+        const float* pbase = p.part + (((size_t)a * p.tile_slots + tslot) * 4 + c) * (BN / 2) * D;
+        return make_buffer(pbase, (uint32_t)((BN / 2) * D * 4));
       };
+      const uint32_t loff = 16 * (uint32_t)lane;
       constexpr int SC1 = 16;  // cache-policy bit: device scope
       int order = 0;
       if (lane == 0) order = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -464,20 +472,15 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       if (order < nsplit - 1) {
         const __amdgpu_buffer_rsrc_t pr = slot_buffer(order);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const int key = kc0 + 32 * ks + l32;
-          if (key < k1) {
-            const uint32_t poff = (uint32_t)((key * D + 4 * g2) * 4);
+        for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+          for (int db = 0; db < DB; ++db)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const f32x4 v = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
-                                 acc[ks][db][4 * i + 3]};
-                __builtin_amdgcn_raw_buffer_store_b128(v, pr, poff + 4 * (db * 32 + 8 * i), 0, SC1);
-              }
-          }
-        }
+            for (int i = 0; i < 4; ++i) {
+              const f32x4 v = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
+                               acc[ks][db][4 * i + 3]};
+              __builtin_amdgcn_raw_buffer_store_b128(v, pr, loff + 1024 * ((ks * DB + db) * 4 + i), 0, SC1);
+            }
         // (slot 0's owner is never read: a part missing from slots 1 .. is in slot 0)
         if (order > 0 && lane == 0) __hip_atomic_store(owner + order, split, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the sums and the owner have reached device scope
@@ -527,11 +530,20 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const int key = kc0 + 32 * ks + l32;
-        if (key < k1) {
-          const uint32_t poff = (uint32_t)((key * D + 4 * g2) * 4);
-          bf16* op = outp + (orow + key) * D + 4 * g2;
 #pragma unroll
-          for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < DB; ++db) {
+          // the other parts' sums of these 16 accumulator entries, loaded
+          // together (every lane: the region is whole even past a ragged end)
+          f32x4 oth[nsplit][4];
+#pragma unroll
+          for (int q = 0; q < nsplit; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (q != split)
+                oth[q][i] = __builtin_amdgcn_raw_buffer_load_b128(slot_buffer(slot_of(q)),
+                                                                  loff + 1024 * ((ks * DB + db) * 4 + i), 0, SC1);
+          if (key < k1) {
+            bf16* op = outp + (orow + key) * D + 4 * g2;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const f32x4 own = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
@@ -539,13 +551,12 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
               f32x4 tot = own;
 #pragma unroll
               for (int q = 0; q < nsplit; ++q) {
-                const f32x4 x = q == split ? own
-                                           : __builtin_amdgcn_raw_buffer_load_b128(
-                                                 slot_buffer(slot_of(q)), poff + 4 * (db * 32 + 8 * i), 0, SC1);
+                const f32x4 x = q == split ? own : oth[q][i];
                 tot = q == 0 ? x : tot + x;
               }
               st_bf16x4(op + db * 32 + 8 * i, tot[0] * sc, tot[1] * sc, tot[2] * sc, tot[3] * sc);
             }
+          }
         }
       }
     } else {
@@ -828,7 +839,7 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   p.part = part;
   p.pair = pair;
   p.seq = s.seq;
-  p.seq_clean_rows = dkdv_clean_rows(s);
+  p.tile_slots = dkdv_tile_slots(s);
   p.L = s.L;
   p.S = s.S;
   p.Hq = s.Hq;

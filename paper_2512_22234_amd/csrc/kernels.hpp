@@ -158,10 +158,16 @@ inline int dkdv_nsplit(int B, int Hkv, int L, const SeqLayout& seq) {
 }
 inline int dkdv_nsplit(const Shape& s) { return dkdv_nsplit(s.B, s.Hkv, s.L, s.seq); }
 // float32 sums of the parts of the clean key tiles' walks that do not finish
-// last: per arrival slot (nsplit - 1 of them) dK and dV, one row per
-// clean-half key.
+// last: per arrival slot (nsplit - 1 of them) and clean key tile (with its
+// sequence and KV head: dkdv_tile_slots of them) a region of 2 x 128 x D
+// floats (dK and dV of the tile's 128 keys, a ragged last tile padded), in
+// the register order of the waves that store and load them.
+inline size_t dkdv_tile_slots(const Shape& s) {
+  return s.seq.cu ? (size_t)packed_rows_bound(s.seq.T, s.B, s.L, DKV_BN) * s.Hkv
+                  : (size_t)((s.L + DKV_BN - 1) / DKV_BN) * s.B * s.Hkv;
+}
 inline size_t dkdv_partial_floats(const Shape& s) {
-  return (size_t)(dkdv_nsplit(s) - 1) * 2 * dkdv_clean_rows(s) * s.D;
+  return (size_t)(dkdv_nsplit(s) - 1) * dkdv_tile_slots(s) * 2 * DKV_BN * s.D;
 }
 // Pairing counters: per (clean key tile, batch x KV head, key group of 32)
 // eight ints: the arrival count, the count of parts that have published their

@@ -154,20 +154,23 @@ def test_workspace_bytes():
 
 def test_workspace_bytes_follow_the_dkdv_split():
     """bf16 backward workspace = (lse2, delta) per query row + float32 sums of
-    nsplit - 1 parts of the clean key tiles' walks (dK and dV, one row per
-    clean-half key) + 32 pairing ints per (clean key tile, sequence x KV head)
-    (each piece rounded up to 256 bytes).  Few KV heads x length (the small
-    configuration) split each walk in four parts, the 8B one in two."""
+    nsplit - 1 parts of the clean key tiles' walks (dK and dV of the 128 keys
+    of every clean key tile and sequence x KV head, a ragged last tile padded)
+    + 32 pairing ints per (clean key tile, sequence x KV head) (each piece
+    rounded up to 256 bytes).  Few KV heads x length (the small configuration)
+    split each walk in four parts, the 8B one in two."""
     f = bd.bd_attn_workspace_bytes
 
     def want(B, L, Hq, Hkv, D, nsplit):
         r256 = lambda x: -(-x // 256) * 256
-        return (r256(B * Hq * 2 * L * 8) + r256((nsplit - 1) * 2 * B * Hkv * L * D * 4)
-                + r256(32 * B * Hkv * (-(-L // 128)) * 4))
+        nkt = -(-L // 128)
+        return (r256(B * Hq * 2 * L * 8) + r256((nsplit - 1) * 2 * B * Hkv * nkt * 128 * D * 4)
+                + r256(32 * B * Hkv * nkt * 4))
 
     assert f(4, 1024, 4, 16, 4, 64, 0, 1) == want(4, 1024, 16, 4, 64, 4) == 26_230_784
     assert f(2, 2048, 4, 32, 8, 128, 0, 1) == want(2, 2048, 32, 8, 128, 2) == 35_684_352
     assert f(1, 8192, 4, 32, 8, 128, 0, 1) == want(1, 8192, 32, 8, 128, 2)
+    assert f(2, 300, 4, 8, 2, 64, 0, 1) == want(2, 300, 8, 2, 64, 4)       # ragged last key tile
 
 
 # Fake, never-dereferenced device addresses: every call below fails validation
