@@ -527,36 +527,40 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       auto slot_of = [&](int q) __attribute__((always_inline)) {
         return q == own_of[1] ? 1 : q == own_of[2] ? 2 : 0;
       };
+      // Output rows kc0 .. k1 - 1 of this tensor through a buffer descriptor
+      // that ends at k1: stores of keys past a ragged end fall outside it and
+      // are dropped, so no branch separates the loads of one group of
+      // accumulator quads from the next and the loads can be issued together.
+      const __amdgpu_buffer_rsrc_t ob =
+          make_buffer(outp + (orow + kc0) * D, (uint32_t)(imax(0, imin(BN / 2, k1 - kc0)) * D * 2));
+      // groups of GQ accumulator quads: the other parts' sums of a group are
+      // loaded together (nsplit - 1 of them per quad)
+      constexpr int GQ = nsplit == 2 ? 8 : 4;
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int key = kc0 + 32 * ks + l32;
+      for (int g0 = 0; g0 < 2 * DB * 4; g0 += GQ) {
+        f32x4 oth[nsplit][GQ];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          // the other parts' sums of these 16 accumulator entries, loaded
-          // together (every lane: the region is whole even past a ragged end)
-          f32x4 oth[nsplit][4];
+        for (int q = 0; q < nsplit; ++q)
 #pragma unroll
-          for (int q = 0; q < nsplit; ++q)
+          for (int u = 0; u < GQ; ++u)
+            if (q != split)
+              oth[q][u] = __builtin_amdgcn_raw_buffer_load_b128(slot_buffer(slot_of(q)), loff + 1024 * (g0 + u), 0, SC1);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (q != split)
-                oth[q][i] = __builtin_amdgcn_raw_buffer_load_b128(slot_buffer(slot_of(q)),
-                                                                  loff + 1024 * ((ks * DB + db) * 4 + i), 0, SC1);
-          if (key < k1) {
-            bf16* op = outp + (orow + key) * D + 4 * g2;
+        for (int u = 0; u < GQ; ++u) {
+          const int qd = g0 + u, ks = qd / (4 * DB), db = (qd / 4) % DB, i = qd % 4;
+          const f32x4 own = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2], acc[ks][db][4 * i + 3]};
+          f32x4 tot = own;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const f32x4 own = {acc[ks][db][4 * i], acc[ks][db][4 * i + 1], acc[ks][db][4 * i + 2],
-                                 acc[ks][db][4 * i + 3]};
-              f32x4 tot = own;
-#pragma unroll
-              for (int q = 0; q < nsplit; ++q) {
-                const f32x4 x = q == split ? own : oth[q][i];
-                tot = q == 0 ? x : tot + x;
-              }
-              st_bf16x4(op + db * 32 + 8 * i, tot[0] * sc, tot[1] * sc, tot[2] * sc, tot[3] * sc);
-            }
+          for (int q = 0; q < nsplit; ++q) {
+            const f32x4 x = q == split ? own : oth[q][u];
+            tot = q == 0 ? x : tot + x;
           }
+          bf16x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = (bf16)(tot[e] * sc);
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, o), ob,
+                                                (uint32_t)(((32 * ks + l32) * D + 32 * db + 8 * i + 4 * g2) * 2), 0, 0);
         }
       }
     } else {
