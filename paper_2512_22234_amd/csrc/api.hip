@@ -320,6 +320,33 @@ int bd_attn_visit_lists_host(int L, int S, int BM, int BN, int by_key_tile, int 
         // the kernel repeats the last position's copy past the end of the walk
         const bd::WalkPos l = wk.last();
         if (wk.steps() > 0 && (l.k != prev.k || l.qh != prev.qh || l.g != prev.g)) return BD_ATTN_ERR_INVALID_ARGUMENT;
+        // positions by index, over one and over three query heads
+        for (int G = 1; G <= 3; G += 2) {
+          const bd::QueryWalk wg = bd::query_walk(kh, j, split, nsplit, L, S, BM, BN, G);
+          bd::WalkPos ps = wg.first();
+          for (int t = 0; t < wg.steps(); ++t, ps.next(wg)) {
+            const bd::WalkPos a = wg.at(t);
+            if (a.k != ps.k || a.qh != ps.qh || a.g != ps.g) return BD_ATTN_ERR_INVALID_ARGUMENT;
+          }
+        }
+        // clean key tiles: for each 32-key group, the first step of the walk
+        // with no visible pair, against a scan of the pair classes
+        if (kh == bd::HALF_CLEAN && BN % 32 == 0) {
+          for (int g = 0; g < BN / 32; ++g) {
+            const int gk0 = k0 + 32 * g, gk1 = bd::imin(k1, gk0 + 32);
+            int want = wk.steps();
+            bd::WalkPos ps = wk.first();
+            for (int t = 0; t < wk.steps(); ++t, ps.next(wk)) {
+              const int q0 = ps.tile(wk) * BM, q1 = bd::imin(L, q0 + BM);
+              if (gk0 >= gk1 || bd::classify_pair(ps.qh, q0, q1, kh, gk0, gk1, S, false) == bd::TILE_EMPTY) {
+                want = t;
+                break;
+              }
+            }
+            if (bd::first_unseen_step(wk, bd::KeyGroupSight(kh, gk0, k1, L, S), BM, L) != want)
+              return BD_ATTN_ERR_INVALID_ARGUMENT;
+          }
+        }
       }
     }
   }

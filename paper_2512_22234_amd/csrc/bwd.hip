@@ -248,7 +248,18 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     const PosWindow win_c = queries_seeing(kh, HALF_CLEAN, kblock0, L, S, kvalid);
     WalkPos cur = first;
     uint32_t bcur = 0;  // byte offset of tile t's buffer (tile t + 1's follows, modulo NBUF)
-    auto step = [&](int t, f32x16& sc, f32x16& dc, f32x16& sn, f32x16& dn) __attribute__((always_inline)) {
+    // Clean key tiles: blocks in which no query sees any key of this group
+    // (on the diagonal, at the end of the walk) are skipped: no scores, and no
+    // P or dS for the consumers, which skip them too.  (The queries seeing a
+    // clean key group also see every earlier group's keys, which the
+    // consumers rely on.)  The steps before the first such block run without
+    // the tests, so that they keep their schedule: the tests split a step's
+    // code into pieces the scores' MFMAs cannot interleave across.
+    const KeyGroupSight sight(kh, k0 + 32 * kg, k1, L, S);
+    const int U = clean ? first_unseen_step(wk, sight, BM, L) : T;  // blocks [0, U) are seen
+    bool vis = U > 0;                                               // block t is seen
+    auto step = [&](int t, f32x16& sc, f32x16& dc, f32x16& sn, f32x16& dn, auto tested)
+                    __attribute__((always_inline)) {
       const int qh = cur.qh, q0 = cur.tile(wk) * BM;
       cur.next(wk);
       const uint32_t bnext = bcur == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcur + Smem::BUF;
@@ -257,13 +268,39 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
       bcur = bnext;
       char* xw = sm.x(t & 1);
       // (EMPTY tiles are never visited; the window test would mask all of one)
-      if (fr.full(qh, q0, BM)) {
-        scores(bn, sn, dn);
-        softmax_grad(bt, xw, sc, dc, 0, 0u, Flag<false>());
+      if constexpr (!decltype(tested)::value) {
+        if (fr.full(qh, q0, BM)) {
+          scores(bn, sn, dn);
+          softmax_grad(bt, xw, sc, dc, 0, 0u, Flag<false>());
+        } else {
+          const PosWindow win = qh == HALF_NOISY ? win_n : win_c;
+          scores(bn, sn, dn);
+          softmax_grad(bt, xw, sc, dc, q0 + 4 * g2 - win.lo, (unsigned)(win.hi - win.lo), Flag<true>());
+        }
       } else {
-        const PosWindow win = qh == HALF_NOISY ? win_n : win_c;
-        scores(bn, sn, dn);
-        softmax_grad(bt, xw, sc, dc, q0 + 4 * g2 - win.lo, (unsigned)(win.hi - win.lo), Flag<true>());
+        const bool vis_t = vis;
+        vis = !clean || sight.sees(cur.qh, cur.tile(wk) * BM, BM, L);  // block t + 1 (past the end: unused)
+        // (each case one straight run of code)
+        if (fr.full(qh, q0, BM)) {
+          if (vis) {
+            scores(bn, sn, dn);
+            softmax_grad(bt, xw, sc, dc, 0, 0u, Flag<false>());
+          } else {
+            softmax_grad(bt, xw, sc, dc, 0, 0u, Flag<false>());
+          }
+        } else {
+          const PosWindow win = qh == HALF_NOISY ? win_n : win_c;
+          const int rel = q0 + 4 * g2 - win.lo;
+          const unsigned span = (unsigned)(win.hi - win.lo);
+          if (vis && vis_t) {
+            scores(bn, sn, dn);
+            softmax_grad(bt, xw, sc, dc, rel, span, Flag<true>());
+          } else if (vis) {
+            scores(bn, sn, dn);
+          } else if (vis_t) {
+            softmax_grad(bt, xw, sc, dc, rel, span, Flag<true>());
+          }
+        }
       }
     };
     if (noisy_diag) {
@@ -284,13 +321,21 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     }
     f32x16 sA, dA, sB, dB;
     __syncthreads();  // the first three query tiles are in LDS
-    if (T > 0) scores(sm.mem, sA, dA);
-    // steps alternate the two accumulator pairs (unrolled by two, no copies)
-    for (int t = 0; t < T; t += 2) {
-      step(t, sA, dA, sB, dB);
+    if (vis) scores(sm.mem, sA, dA);
+    // steps alternate the two accumulator pairs (unrolled by two, no copies);
+    // untested steps t need blocks t and t + 1 seen (an even number of them)
+    const int E = imax(0, U - 1) & ~1;
+    for (int t = 0; t < E; t += 2) {
+      step(t, sA, dA, sB, dB, Flag<false>());
+      barrier_lds_only();
+      step(t + 1, sB, dB, sA, dA, Flag<false>());
+      barrier_lds_only();
+    }
+    for (int t = E; t < T; t += 2) {
+      step(t, sA, dA, sB, dB, Flag<true>());
       barrier_lds_only();
       if (t + 1 < T) {
-        step(t + 1, sB, dB, sA, dA);
+        step(t + 1, sB, dB, sA, dA, Flag<true>());
         barrier_lds_only();
       }
     }
@@ -393,40 +438,68 @@ __global__ __launch_bounds__(512, 1) void dkdv_kernel(DkvParams p) {
     // compiler does not wait for the copy in flight before the reads.
     //   dV^T[d][key] += sum_q dO^T[d][q] P[q][key]   (dV consumers)
     //   dK^T[d][key] += sum_q Q^T[d][q] dS[q][key]   (dK consumers)
-    auto consume = [&](const char* __restrict__ bc, const char* __restrict__ xr, char* __restrict__ bn, int t)
-                       __attribute__((always_inline)) {
-      if (t > 0) {
-        bf16x8 xb[2][2];  // [key group][16-query half]
+    // The products of key group 2 (c % 2) + ks skip the blocks its producer
+    // skipped (clean key tiles; a block the second group is seen in is seen by
+    // the first too).  Blocks before the first one the second group is not
+    // seen in need no test.
+    const KeyGroupSight sight0(kh, kc0, k1, L, S), sight1(kh, kc0 + 32, k1, L, S);
+    const int U1 = clean ? first_unseen_step(wk, sight1, BM, L) : T;  // blocks [0, U1) are seen by both
+    WalkPos cc = U1 < T ? wk.at(U1) : first;                          // block of step t - 1 (tested steps)
+    auto products = [&](const char* __restrict__ bc, const char* __restrict__ xr, auto use0, auto use1)
+                        __attribute__((always_inline)) {
+      constexpr bool u0 = decltype(use0)::value, u1 = decltype(use1)::value;
+      bf16x8 xb[2][2];  // [key group][16-query half]
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-          for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
+          if (ks == 0 ? u0 : u1)
             xb[ks][h] = *reinterpret_cast<const bf16x8*>(xr + (2 * (c & 1) + ks) * Smem::XGRP + 16 * lane +
                                                          (2 * h + xsel) * 1024);
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16x8 a = lds_tr<D>(bc + aoff, ops.tr_rel0, ops.tr_rel1, h, db);
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) acc[ks][db] = mfma32(a, xb[ks][h], acc[ks][db]);
-          }
+        for (int db = 0; db < DB; ++db) {
+          const bf16x8 a = lds_tr<D>(bc + aoff, ops.tr_rel0, ops.tr_rel1, h, db);
+          if constexpr (u0) acc[0][db] = mfma32(a, xb[0][h], acc[0][db]);
+          if constexpr (u1) acc[1][db] = mfma32(a, xb[1][h], acc[1][db]);
+        }
+    };
+    auto consume = [&](const char* __restrict__ bc, const char* __restrict__ xr, char* __restrict__ bn, int t,
+                       auto tested) __attribute__((always_inline)) {
+      if constexpr (!decltype(tested)::value) {
+        if (t > 0) products(bc, xr, Flag<true>(), Flag<true>());
         issue(t + 3 < T ? cp : last, bn);
       } else {
-        issue(t + 3 < T ? cp : last, bn);
+        // (t > 0; each case one straight run of code)
+        const int qc = cc.tile(wk) * BM;
+        const bool v0 = !clean || sight0.sees(cc.qh, qc, BM, L), v1 = !clean || sight1.sees(cc.qh, qc, BM, L);
+        cc.next(wk);
+        if (v1) {
+          products(bc, xr, Flag<true>(), Flag<true>());
+          issue(t + 3 < T ? cp : last, bn);
+        } else if (v0) {
+          products(bc, xr, Flag<true>(), Flag<false>());
+          issue(t + 3 < T ? cp : last, bn);
+        } else {
+          issue(t + 3 < T ? cp : last, bn);
+        }
       }
     };
     uint32_t bcons = (Smem::NBUF - 1) * Smem::BUF;  // buffer of tile t - 1
     uint32_t bcopy = 3 * Smem::BUF;                  // buffer tile t + 3 is copied into
-    for (int t = 0; t < steps; ++t) {
-      consume(sm.mem + bcons, sm.x((t + 1) & 1), sm.mem + bcopy, t);
+    auto consumer_step = [&](int t, auto tested) __attribute__((always_inline)) {
+      consume(sm.mem + bcons, sm.x((t + 1) & 1), sm.mem + bcopy, t, tested);
       bcons = bcons == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcons + Smem::BUF;
       bcopy = bcopy == (Smem::NBUF - 1) * Smem::BUF ? 0u : bcopy + Smem::BUF;
       if (t + 3 < T) cp.next(wk);
       compute_fence();
       wait_global_loads_but<NC>();  // tile t + 2 has landed (the copy issued this step may not have)
       barrier_lds_only();           // ... in every wave's part; the copy in flight stays in flight
-    }
+    };
+    const int E = imin(steps, U1 + 1);  // steps whose block t - 1 < U1
+    for (int t = 0; t < E; ++t) consumer_step(t, Flag<false>());
+    for (int t = E; t < steps; ++t) consumer_step(t, Flag<true>());
     }
     wait_global_loads();  // no copy may still be writing LDS when the workgroup ends
 

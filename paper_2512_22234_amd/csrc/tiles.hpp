@@ -197,6 +197,20 @@ BD_HD PosWindow wave_queries_seeing(int kh, int qh, int r0, int r1, int L, int S
   return kh == HALF_CLEAN ? PosWindow{a0, L} : PosWindow{0, 0};
 }
 
+// The queries of each half that see some key of the group [r0, min(r0 + 32,
+// k1)) of half kh (one wave's keys in the dK/dV kernel; empty past k1).
+struct KeyGroupSight {
+  PosWindow n, c;
+  BD_HD KeyGroupSight(int kh, int r0, int k1, int L, int S)
+      : n(wave_queries_seeing(kh, HALF_NOISY, r0, imin(k1, r0 + 32), L, S)),
+        c(wave_queries_seeing(kh, HALF_CLEAN, r0, imin(k1, r0 + 32), L, S)) {}
+  // whether some query of [q0, min(L, q0 + nq)) of half qh sees one of the keys
+  BD_HD bool sees(int qh, int q0, int nq, int L) const {
+    const PosWindow v = qh == HALF_NOISY ? n : c;
+    return v.lo < v.hi && q0 < v.hi && imin(L, q0 + nq) > v.lo;
+  }
+};
+
 // Key tiles visited by query tile (qh, i): clean key tiles [0, nclean) then,
 // for a noisy query tile, noisy key tiles [noisy0, noisy0 + nnoisy).
 struct KeyTileList {
@@ -275,6 +289,7 @@ struct QueryWalk {
   BD_HD int steps() const { return G * (K + K2); }
   BD_HD WalkPos first() const;
   BD_HD WalkPos last() const;
+  BD_HD WalkPos at(int idx) const;  // the idx-th position (0 <= idx < steps())
 };
 // Position (walk tile k, half qh, query head g) in a QueryWalk.
 struct WalkPos {
@@ -294,6 +309,15 @@ struct WalkPos {
 BD_HD WalkPos QueryWalk::first() const { return WalkPos{0, K2 > 0 ? HALF_NOISY : rest, 0}; }
 BD_HD WalkPos QueryWalk::last() const {
   return K > K2 ? WalkPos{K - 1, rest, G - 1} : WalkPos{K2 - 1, HALF_CLEAN, G - 1};
+}
+BD_HD WalkPos QueryWalk::at(int idx) const {
+  const int n2 = 2 * G * K2;  // steps of the tiles with both halves
+  if (idx < n2) {
+    const int k = idx / (2 * G), r = idx - k * 2 * G;
+    return r < G ? WalkPos{k, HALF_NOISY, r} : WalkPos{k, HALF_CLEAN, r - G};
+  }
+  const int r = idx - n2, k = K2 + r / G;
+  return WalkPos{k, rest, r - (k - K2) * G};
 }
 
 // Walk of key tile (kh, j).  A clean key tile is seen by noisy query tiles
@@ -324,6 +348,23 @@ BD_HD QueryWalk query_walk(int kh, int j, int split, int nsplit, int L, int S, i
     wk.rest = HALF_NOISY;
   }
   return wk;
+}
+
+// The first step of walk wk (query blocks of BM rows) in which no query sees
+// any key of a group, steps() if there is none: every earlier block has a
+// visible pair with the group.  Visibility depends on the tile and half only,
+// so the scan takes one or two tests per walk tile.
+BD_HD int first_unseen_step(const QueryWalk& wk, const KeyGroupSight& sight, int BM, int L) {
+  for (int k = 0; k < wk.K; ++k) {
+    const int q0 = (wk.u0 + wk.du * k) * BM;
+    if (k < wk.K2) {
+      if (!sight.sees(HALF_NOISY, q0, BM, L)) return 2 * wk.G * k;
+      if (!sight.sees(HALF_CLEAN, q0, BM, L)) return 2 * wk.G * k + wk.G;
+    } else if (!sight.sees(wk.rest, q0, BM, L)) {
+      return 2 * wk.G * wk.K2 + wk.G * (k - wk.K2);
+    }
+  }
+  return wk.steps();
 }
 
 }  // namespace bd

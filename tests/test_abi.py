@@ -133,6 +133,20 @@ def test_run_windows_are_the_union_of_row_masks(by_key):
                 np.testing.assert_array_equal(got, want, err_msg=f"L={L} S={S} group={group}")
 
 
+def test_clean_key_groups_are_seen_by_nested_query_sets():
+    """The dK/dV kernel skips the blocks of a 32-key group that no query sees;
+    its consumer waves, which take two adjacent groups, rely on every query
+    that sees a clean key group also seeing the group before it (checked on
+    the oracle's mask, run by run)."""
+    for L in (1, 3, 8, 31, 33, 64, 100, 200):
+        for S in sorted({1, 2, 3, 4, 5, 8, 16, 32, 33, 64, L, L + 1}):
+            M = oracle.visibility_mask(L, S).T  # rows: keys, columns: queries that see them
+            for r0 in range(0, L - 32, 32):
+                first = M[L + r0:L + r0 + 32].any(axis=0)
+                second = M[L + r0 + 32:L + min(L, r0 + 64)].any(axis=0)
+                assert not (second & ~first).any(), f"L={L} S={S} r0={r0}"
+
+
 def test_classifier_tile_counts_8b_shape():
     # L=2048, S=4 with 128x128 tiles: per (b, h) 1024 pairs; 240 FULL, 48 PARTIAL, 736 EMPTY
     c = bd.bd_attn_classify_tiles_host(2048, 4, 128, 128)
