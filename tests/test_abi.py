@@ -187,6 +187,26 @@ def test_workspace_bytes_follow_the_dkdv_split():
     assert f(2, 300, 4, 8, 2, 64, 0, 1) == want(2, 300, 8, 2, 64, 4)       # ragged last key tile
 
 
+def test_varlen_workspace_bytes_follow_the_dkdv_split():
+    """bf16 packed backward workspace = (lse2, delta) per query row + float32 sums
+    of nsplit - 1 parts of the clean key tiles' walks (a bound on the key
+    tiles of all sequences, T/128 + n, at most n * cdiv(max_L, 128), times
+    Hkv; 2 x 128 x D floats each) + the pairing counters (n x Hkv x
+    cdiv(max_L, 128) key tiles, 32 ints each)."""
+    f = bd.bd_attn_varlen_workspace_bytes
+    r256 = lambda x: -(-x // 256) * 256
+
+    def want(n, T, maxL, Hq, Hkv, D, nsplit):
+        nkt = -(-maxL // 128)
+        slots = min(T // 128 + n, n * nkt) * Hkv
+        return r256(Hq * 2 * T * 8) + r256((nsplit - 1) * slots * 2 * 128 * D * 4) + r256(32 * n * Hkv * nkt * 4)
+
+    # the measured packed workload (6 sequences, 4096 tokens, longest 1701): two parts
+    assert f(6, 4096, 1701, 4, 32, 8, 128, 0, 1) == want(6, 4096, 1701, 32, 8, 128, 2)
+    # few KV heads x tokens: four parts
+    assert f(3, 600, 300, 4, 8, 2, 64, 0, 1) == want(3, 600, 300, 8, 2, 64, 4)
+
+
 # Fake, never-dereferenced device addresses: every call below fails validation
 # and returns before any HIP call (the defaults use the float32 path so that
 # the workspace is non-empty and the workspace checks are exercised).
