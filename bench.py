@@ -15,8 +15,9 @@ value  = effective TFLOP/s counting only visible (query, key) pairs:
          (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
          visible pair, the FlashAttention convention).
 roofline: the dominant kernel's algorithmic FLOPs per launch over its average
-         duration, from events recorded around every kernel launch of the timed
-         steps, against the bf16 dense MFMA peak.
+         duration, from events that every kernel dispatch of the timed steps
+         records as it begins and ends (no packets of their own between the
+         kernels), against the bf16 dense MFMA peak.
 kernels: per kernel the event-timed duration and algorithmic rate, and, from
          the committed rocprofv3 counter record of the same kernel sources
          (profiles/bd_attn_8b_counters.md), the executed MFMA rate over this
@@ -382,7 +383,7 @@ def main():
                       device=dev)
     fwd_names = bd.bd_attn_stage_names(False, code)
     bwd_names = bd.bd_attn_stage_names(True, code)
-    nf, nb = len(fwd_names) + 1, len(bwd_names) + 1
+    nf, nb = 2 * len(fwd_names), 2 * len(bwd_names)  # each kernel's start and end, from its dispatch
     K = args.steps
     fwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nf)] for _ in range(K)]
     bwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nb)] for _ in range(K)]
@@ -426,11 +427,12 @@ def main():
     log(f"[bench] timed region: {ms:.4f} ms/step (events), {wall * 1e3 / K:.4f} ms/step (host clock)")
 
     # per-kernel durations from the marks (mean over the timed steps), and the
-    # per-step fwd / bwd durations (median over the timed steps)
+    # per-step fwd / bwd durations, first kernel's start to last kernel's end
+    # (median over the timed steps)
     per = {}
     for names, marks in ((fwd_names, fwd_marks), (bwd_names, bwd_marks)):
         for j, name in enumerate(names):
-            per[name] = sum(m[j].elapsed_time(m[j + 1]) for m in marks) / K
+            per[name] = sum(m[2 * j].elapsed_time(m[2 * j + 1]) for m in marks) / K
     t_fwd = sum(per[n] for n in fwd_names)
     t_bwd = sum(per[n] for n in bwd_names)
     step_ms = sorted(f[0].elapsed_time(f[-1]) + b[0].elapsed_time(b[-1]) for f, b in zip(fwd_marks, bwd_marks))

@@ -189,11 +189,14 @@ int bd_attn_group_windows_host(int L, int S, int by_key, int group, int8_t* out)
 
 /*
  * Benchmark variants of bd_attn_fwd / bd_attn_bwd: identical work and
- * validation, and in addition hipEventRecord(marks[i], stream) for caller-
- * created events: marks[0] before the first kernel launch and marks[i] right
- * after launch i, for as many marks as n_marks allows.  The kernels launched,
- * in order, are named by bd_attn_stage_names.  Intended for measuring each
- * kernel's duration on the stream it runs on.
+ * validation, and in addition caller-created events recorded from the kernel
+ * dispatches themselves (hipExtLaunchKernelGGL): kernel launch i records
+ * marks[2i] as it begins and marks[2i + 1] as it ends, for as many launches
+ * as n_marks covers (n_marks = 2 x the launches for all of them).  The
+ * events put no packet of their own in the stream, so the kernels follow
+ * each other as in the plain calls.  The kernels launched, in order, are
+ * named by bd_attn_stage_names.  Intended for measuring each kernel's
+ * duration on the stream it runs on.
  */
 int bd_attn_fwd_marked(const void* Q, const void* K, const void* V,
                        int B, int L, int S, int Hq, int Hkv, int D, float scale, int dtype,

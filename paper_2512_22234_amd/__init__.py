@@ -140,13 +140,13 @@ def bd_attn_stage_names(for_bwd: bool, dtype: int = BD_ATTN_BF16):
 
 def bd_attn_fwd_marked(q, k, v, L: int, S: int, marks, scale=None, out=None, lse=None, workspace=None,
                        stream=None):
-    """bd_attn_fwd that also records marks[0] before and marks[i] after kernel i."""
+    """bd_attn_fwd that also records marks[2i] and marks[2i + 1] as kernel i begins and ends."""
     return bd_attn_fwd(q, k, v, L, S, scale, out, lse, workspace, stream, _marks=marks)
 
 
 def bd_attn_bwd_marked(do, q, k, v, o, lse, L: int, S: int, marks, scale=None, dq=None, dk=None, dv=None,
                        workspace=None, stream=None):
-    """bd_attn_bwd that also records marks[0] before and marks[i] after kernel i."""
+    """bd_attn_bwd that also records marks[2i] and marks[2i + 1] as kernel i begins and ends."""
     return bd_attn_bwd(do, q, k, v, o, lse, L, S, scale, dq, dk, dv, workspace, stream, _marks=marks)
 
 

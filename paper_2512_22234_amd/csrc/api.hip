@@ -166,20 +166,21 @@ int validate_lce(int N, int V, int Dm, int dtype, bd::LceShape& s) {
     if ((expr) != hipSuccess) return BD_ATTN_ERR_HIP;   \
   } while (0)
 
-#define BD_LAUNCH(expr)                                                     \
-  do {                                                                      \
-    if ((expr) != hipSuccess || marks.rec(stream) != hipSuccess) return BD_ATTN_ERR_HIP; \
-  } while (0)
-
-// Optional caller-owned events recorded on the stream: mark 0 before the first
-// launch, mark i after launch i (benchmark entry points only).
+// Optional caller-owned events (benchmark entry points only): launch i
+// records marks 2i and 2i + 1 from its own dispatch, as the kernel begins and
+// as it ends, so the marks add nothing to the queue between the kernels.
 struct Marks {
   hipEvent_t* ev;
   int n;
   int i = 0;
-  hipError_t rec(hipStream_t st) {
-    if (ev == nullptr || i >= n) return hipSuccess;
-    return hipEventRecord(ev[i++], st);
+  bd::LaunchEvents next() {
+    bd::LaunchEvents e;
+    if (ev != nullptr && 2 * i + 1 < n) {
+      e.start = ev[2 * i];
+      e.stop = ev[2 * i + 1];
+    }
+    ++i;
+    return e;
   }
 };
 
@@ -622,21 +623,20 @@ int fwd_impl(const bd::Shape& s, const void* Q, const void* K, const void* V, in
     return BD_ATTN_ERR_INVALID_ARGUMENT;
 
   (void)hipGetLastError();  // clear a stale error so it is not reported as ours
-  BD_TRY(marks.rec(stream));
   char* wb = static_cast<char*>(ws);
   const void *q = Q, *k = K, *v = V;
   void* o = O;
   if (dtype == BD_ATTN_FP32) {
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream, marks.next()));
     q = wb + w.q;
     k = wb + w.k;
     v = wb + w.v;
     o = wb + w.o;
   }
-  BD_LAUNCH(bd::launch_fwd(s, q, k, v, o, LSE, stream));
-  if (dtype == BD_ATTN_FP32) BD_LAUNCH(bd::launch_cast_bf16_to_f32(o, static_cast<float*>(O), nq, stream));
+  BD_TRY(bd::launch_fwd(s, q, k, v, o, LSE, stream, marks.next()));
+  if (dtype == BD_ATTN_FP32) BD_TRY(bd::launch_cast_bf16_to_f32(o, static_cast<float*>(O), nq, stream, marks.next()));
   return BD_ATTN_OK;
 }
 
@@ -664,16 +664,15 @@ int bwd_impl(const bd::Shape& s, const void* dO, const void* Q, const void* K, c
       if (overlap(out[a], out[c])) return BD_ATTN_ERR_INVALID_ARGUMENT;
 
   (void)hipGetLastError();
-  BD_TRY(marks.rec(stream));
   char* wb = static_cast<char*>(ws);
   const void *q = Q, *k = K, *v = V, *o = O, *g = dO;
   void *dq = dQ, *dk = dK, *dv = dV;
   if (dtype == BD_ATTN_FP32) {
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(O), wb + w.o, nq, stream));
-    BD_LAUNCH(bd::launch_cast_f32_to_bf16(static_cast<const float*>(dO), wb + w.dout, nq, stream));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(Q), wb + w.q, nq, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(K), wb + w.k, nk, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(V), wb + w.v, nk, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(O), wb + w.o, nq, stream, marks.next()));
+    BD_TRY(bd::launch_cast_f32_to_bf16(static_cast<const float*>(dO), wb + w.dout, nq, stream, marks.next()));
     q = wb + w.q;
     k = wb + w.k;
     v = wb + w.v;
@@ -686,12 +685,12 @@ int bwd_impl(const bd::Shape& s, const void* dO, const void* Q, const void* K, c
   float* rs = reinterpret_cast<float*>(wb + w.rs);
   float* part = reinterpret_cast<float*>(wb + w.part);
   int* pair = reinterpret_cast<int*>(wb + w.pair);
-  BD_LAUNCH(bd::launch_bwd_dq(s, q, k, v, g, o, LSE, rs, pair, dq, stream));
-  BD_LAUNCH(bd::launch_bwd_dkdv(s, q, k, v, g, rs, dk, dv, part, pair, stream));
+  BD_TRY(bd::launch_bwd_dq(s, q, k, v, g, o, LSE, rs, pair, dq, stream, marks.next()));
+  BD_TRY(bd::launch_bwd_dkdv(s, q, k, v, g, rs, dk, dv, part, pair, stream, marks.next()));
   if (dtype == BD_ATTN_FP32) {
-    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream));
-    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream));
-    BD_LAUNCH(bd::launch_cast_bf16_to_f32(dv, static_cast<float*>(dV), nk, stream));
+    BD_TRY(bd::launch_cast_bf16_to_f32(dq, static_cast<float*>(dQ), nq, stream, marks.next()));
+    BD_TRY(bd::launch_cast_bf16_to_f32(dk, static_cast<float*>(dK), nk, stream, marks.next()));
+    BD_TRY(bd::launch_cast_bf16_to_f32(dv, static_cast<float*>(dV), nk, stream, marks.next()));
   }
   return BD_ATTN_OK;
 }

@@ -26,13 +26,15 @@ unsigned cast_grid(size_t n) {
 
 }  // namespace
 
-hipError_t launch_cast_f32_to_bf16(const float* x, void* y, size_t n, hipStream_t st) {
-  hipLaunchKernelGGL(cast_f32_bf16_kernel, dim3(cast_grid(n)), dim3(256), 0, st, x, static_cast<bf16*>(y), n);
+hipError_t launch_cast_f32_to_bf16(const float* x, void* y, size_t n, hipStream_t st, LaunchEvents ev) {
+  hipExtLaunchKernelGGL(cast_f32_bf16_kernel, dim3(cast_grid(n)), dim3(256), 0, st, ev.start, ev.stop, 0, x,
+                        static_cast<bf16*>(y), n);
   return hipGetLastError();
 }
 
-hipError_t launch_cast_bf16_to_f32(const void* x, float* y, size_t n, hipStream_t st) {
-  hipLaunchKernelGGL(cast_bf16_f32_kernel, dim3(cast_grid(n)), dim3(256), 0, st, static_cast<const bf16*>(x), y, n);
+hipError_t launch_cast_bf16_to_f32(const void* x, float* y, size_t n, hipStream_t st, LaunchEvents ev) {
+  hipExtLaunchKernelGGL(cast_bf16_f32_kernel, dim3(cast_grid(n)), dim3(256), 0, st, ev.start, ev.stop, 0,
+                        static_cast<const bf16*>(x), y, n);
   return hipGetLastError();
 }
 

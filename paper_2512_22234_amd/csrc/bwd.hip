@@ -904,7 +904,8 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(DqParams p) {
 
 template <int D>
 hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st) {
+                         const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st,
+                         LaunchEvents ev) {
   DkvParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
@@ -930,16 +931,16 @@ hipError_t launch_dkdv_d(const Shape& s, const void* Q, const void* K, const voi
   // (packed sequences: grid sized by a bound on the key tiles of all sequences)
   const int rows = s.seq.cu ? packed_rows_bound(s.seq.T, s.B, s.L, DKV_BN) : p.nKT * s.B;
   if (dkdv_nsplit(s) == 4) {
-    hipLaunchKernelGGL((dkdv_kernel<D, 4>), dim3(5 * rows * s.Hkv), dim3(512), 0, st, p);
+    hipExtLaunchKernelGGL((dkdv_kernel<D, 4>), dim3(5 * rows * s.Hkv), dim3(512), 0, st, ev.start, ev.stop, 0, p);
   } else {
-    hipLaunchKernelGGL((dkdv_kernel<D, 2>), dim3(3 * rows * s.Hkv), dim3(512), 0, st, p);
+    hipExtLaunchKernelGGL((dkdv_kernel<D, 2>), dim3(3 * rows * s.Hkv), dim3(512), 0, st, ev.start, ev.stop, 0, p);
   }
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void* V, const void* dO, const void* O,
-                       const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st) {
+                       const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st, LaunchEvents ev) {
   DqParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
@@ -962,22 +963,23 @@ hipError_t launch_dq_d(const Shape& s, const void* Q, const void* K, const void*
   p.c = s.scale * LOG2E;
   p.scale = s.scale;
   const dim3 grid(2 * p.nQT * p.nbh);
-  hipLaunchKernelGGL(dq_kernel<D>, grid, dim3(256), 0, st, p);
+  hipExtLaunchKernelGGL(dq_kernel<D>, grid, dim3(256), 0, st, ev.start, ev.stop, 0, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                           const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st) {
-  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, rs, dK, dV, part, pair, st);
-  return launch_dkdv_d<64>(s, Q, K, V, dO, rs, dK, dV, part, pair, st);
+                           const float* rs, void* dK, void* dV, float* part, int* pair, hipStream_t st,
+                           LaunchEvents ev) {
+  if (s.D == 128) return launch_dkdv_d<128>(s, Q, K, V, dO, rs, dK, dV, part, pair, st, ev);
+  return launch_dkdv_d<64>(s, Q, K, V, dO, rs, dK, dV, part, pair, st, ev);
 }
 
 hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO, const void* O,
-                         const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st) {
-  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st);
-  return launch_dq_d<64>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st);
+                         const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st, LaunchEvents ev) {
+  if (s.D == 128) return launch_dq_d<128>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st, ev);
+  return launch_dq_d<64>(s, Q, K, V, dO, O, LSE, rs, pair, dQ, st, ev);
 }
 
 }  // namespace bd

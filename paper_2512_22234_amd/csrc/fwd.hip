@@ -349,7 +349,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdParams p) {
 
 template <int D>
 hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void* V, void* O,
-                        float* LSE, hipStream_t st) {
+                        float* LSE, hipStream_t st, LaunchEvents ev) {
   FwdParams p;
   p.Q = static_cast<const bf16*>(Q);
   p.K = static_cast<const bf16*>(K);
@@ -366,16 +366,16 @@ hipError_t launch_fwd_d(const Shape& s, const void* Q, const void* K, const void
   p.nbh = s.B * s.Hq;
   p.c = s.scale * LOG2E;
   const dim3 grid(2 * p.nQT * p.nbh);
-  hipLaunchKernelGGL(fwd_kernel<D>, grid, dim3(256), 0, st, p);
+  hipExtLaunchKernelGGL(fwd_kernel<D>, grid, dim3(256), 0, st, ev.start, ev.stop, 0, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* V, void* O,
-                      float* LSE, hipStream_t st) {
-  if (s.D == 128) return launch_fwd_d<128>(s, Q, K, V, O, LSE, st);
-  return launch_fwd_d<64>(s, Q, K, V, O, LSE, st);
+                      float* LSE, hipStream_t st, LaunchEvents ev) {
+  if (s.D == 128) return launch_fwd_d<128>(s, Q, K, V, O, LSE, st, ev);
+  return launch_fwd_d<64>(s, Q, K, V, O, LSE, st, ev);
 }
 
 }  // namespace bd

@@ -2,6 +2,8 @@
 // kernel translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
@@ -116,11 +118,18 @@ constexpr int DQ_BM = 128, DQ_BN = 64;
 // dK/dV tiles: BN keys per workgroup (4 key groups x 32), BM queries per step.
 constexpr int DKV_BN = 128, DKV_BM = 32;
 
-hipError_t launch_cast_f32_to_bf16(const float* x, void* y, size_t n, hipStream_t st);
-hipError_t launch_cast_bf16_to_f32(const void* x, float* y, size_t n, hipStream_t st);
+// Events a launch records from its own dispatch packet (hipExtLaunchKernelGGL):
+// `start` as the kernel begins and `stop` as it ends, with no packet of their
+// own in the queue; null events are not recorded.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
+hipError_t launch_cast_f32_to_bf16(const float* x, void* y, size_t n, hipStream_t st, LaunchEvents ev = {});
+hipError_t launch_cast_bf16_to_f32(const void* x, float* y, size_t n, hipStream_t st, LaunchEvents ev = {});
 
 hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* V,
-                      void* O, float* LSE, hipStream_t st);
+                      void* O, float* LSE, hipStream_t st, LaunchEvents ev = {});
 
 // Backward, in launch order:
 //   dq:   dQ, and per query row the float32 pair (lse2, delta) =
@@ -130,10 +139,11 @@ hipError_t launch_fwd(const Shape& s, const void* Q, const void* K, const void* 
 //         every part but the last to finish leaves float32 sums in `part`
 //         (dkdv_partial_floats elements), the last adds them to its own.
 hipError_t launch_bwd_dq(const Shape& s, const void* Q, const void* K, const void* V, const void* dO,
-                         const void* O, const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st);
+                         const void* O, const float* LSE, float* rs, int* pair, void* dQ, hipStream_t st,
+                         LaunchEvents ev = {});
 hipError_t launch_bwd_dkdv(const Shape& s, const void* Q, const void* K, const void* V,
                            const void* dO, const float* rs, void* dK, void* dV, float* part, int* pair,
-                           hipStream_t st);
+                           hipStream_t st, LaunchEvents ev = {});
 
 // Clean-half key rows of every sequence and KV head: B*Hkv*L for fixed
 // length, Hkv*T packed.  Row khead / 2 + k is key k of the clean half of the
