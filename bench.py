@@ -15,9 +15,9 @@ value  = effective TFLOP/s counting only visible (query, key) pairs:
          (4 + 10) * D * N_visible * B * Hq per step (forward 4D, backward 10D per
          visible pair, the FlashAttention convention).
 roofline: the dominant kernel's algorithmic FLOPs per launch over its average
-         duration, from events that every kernel dispatch of the timed steps
-         records as it begins and ends (no packets of their own between the
-         kernels), against the bf16 dense MFMA peak.
+         duration, from events that its dispatches record as they begin and
+         end (no packets of their own between the kernels) in every fourth
+         timed step, against the bf16 dense MFMA peak.
 kernels: per kernel the event-timed duration and algorithmic rate, and, from
          the committed rocprofv3 counter record of the same kernel sources
          (profiles/bd_attn_8b_counters.md), the executed MFMA rate over this
@@ -71,6 +71,7 @@ def log(msg: str):
 
 
 HERE = os.path.dirname(os.path.abspath(__file__))
+MARK_EVERY = 4  # timed steps per step that records the per-kernel dispatch events
 COUNTERS_FILE = os.path.join(HERE, "profiles", "bd_attn_8b_counters.md")
 
 
@@ -385,20 +386,25 @@ def main():
     bwd_names = bd.bd_attn_stage_names(True, code)
     nf, nb = 2 * len(fwd_names), 2 * len(bwd_names)  # each kernel's start and end, from its dispatch
     K = args.steps
-    fwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nf)] for _ in range(K)]
-    bwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nb)] for _ in range(K)]
+    # Every MARK_EVERY-th timed step carries the dispatch events the per-kernel
+    # durations come from; the others run the same calls unmarked (the events
+    # cost ~15 us per marked 8B step, which the step time then includes).
+    marked = [i for i in range(K) if i % MARK_EVERY == 0]
+    fwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nf)] for _ in marked]
+    bwd_marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nb)] for _ in marked]
     for evs in fwd_marks + bwd_marks:   # create the events before the timed region
         for e in evs:
             e.record()
     torch.cuda.synchronize()
 
     def step(i=None):
-        if i is None:
+        if i is None or i % MARK_EVERY:
             bd.bd_attn_fwd(q, k, v, L, S, out=o, lse=lse, workspace=wsf)
             bd.bd_attn_bwd(do, q, k, v, o, lse, L, S, dq=dq, dk=dk, dv=dv, workspace=wsb)
         else:
-            bd.bd_attn_fwd_marked(q, k, v, L, S, fwd_marks[i], out=o, lse=lse, workspace=wsf)
-            bd.bd_attn_bwd_marked(do, q, k, v, o, lse, L, S, bwd_marks[i], dq=dq, dk=dk, dv=dv, workspace=wsb)
+            u = i // MARK_EVERY
+            bd.bd_attn_fwd_marked(q, k, v, L, S, fwd_marks[u], out=o, lse=lse, workspace=wsf)
+            bd.bd_attn_bwd_marked(do, q, k, v, o, lse, L, S, bwd_marks[u], dq=dq, dk=dk, dv=dv, workspace=wsb)
 
     # Clock settle: the GPU's clocks settle only after tens of milliseconds of
     # sustained load, so before the W warm-up steps the step runs for a fixed
@@ -426,13 +432,13 @@ def main():
     ms = start.elapsed_time(end) / K
     log(f"[bench] timed region: {ms:.4f} ms/step (events), {wall * 1e3 / K:.4f} ms/step (host clock)")
 
-    # per-kernel durations from the marks (mean over the timed steps), and the
-    # per-step fwd / bwd durations, first kernel's start to last kernel's end
-    # (median over the timed steps)
+    # per-kernel durations from the marks (mean over the marked timed steps),
+    # and the per-step fwd / bwd durations, first kernel's start to last
+    # kernel's end (median over the marked timed steps)
     per = {}
     for names, marks in ((fwd_names, fwd_marks), (bwd_names, bwd_marks)):
         for j, name in enumerate(names):
-            per[name] = sum(m[2 * j].elapsed_time(m[2 * j + 1]) for m in marks) / K
+            per[name] = sum(m[2 * j].elapsed_time(m[2 * j + 1]) for m in marks) / len(marks)
     t_fwd = sum(per[n] for n in fwd_names)
     t_bwd = sum(per[n] for n in bwd_names)
     step_ms = sorted(f[0].elapsed_time(f[-1]) + b[0].elapsed_time(b[-1]) for f, b in zip(fwd_marks, bwd_marks))
